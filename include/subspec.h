@@ -1,0 +1,164 @@
+/*
+ * subspec.h -- C ABI of the MI355X (gfx950) low-bit substitute-layer library.
+ *
+ * SubSpec (Sec. 4.1, "Quantized Substitute Weights for Offloaded Layers") keeps a
+ * GPU-resident, data-free, group-wise quantized copy of every offloaded linear
+ * layer of the target model and evaluates the draft model with those copies.  The
+ * draft forward (Sec. 4.2) runs on the k leaf tokens of a speculative tree, so each
+ * substitute layer is a linear layer evaluated on a small token batch M against the
+ * full K x N weight.  Sec. 5.1 uses 4-bit codes with groups of 64; this library
+ * also takes 3- and 2-bit codes and groups of 128 (the lower bit widths are named
+ * as future work in the paper's Limitations section).
+ *
+ * The operation, for every output row m < M and column n < N:
+ *     y[m][n] = sum_k x[m][k] * s[g][n] * (q[n][k] - z[g][n]),   g = k / group
+ * with bf16 activations x, unsigned `bits`-bit codes q, fp16 scale s and fp16
+ * (fractional) zero-point z per group of `group` consecutive k of one column, fp32
+ * accumulation and a bf16 result rounded to nearest-even.
+ *
+ * Conventions shared by every entry point
+ *  - Pointers named "device" are HIP device memory owned by the caller; "host" are
+ *    ordinary host memory.  No call frees or retains caller memory.
+ *  - Calls taking a hipStream_t are asynchronous on that stream (0 = the null
+ *    stream).  Argument errors are reported synchronously, before anything is
+ *    enqueued.  A kernel fault surfaces at the caller's next synchronisation.
+ *  - Return value: SUBSPEC_OK or a negative status; subspec_last_error() then
+ *    describes the failure (thread-local, valid until the next failing call).
+ *  - bits in {2,3,4}; group in {64,128}; K % 128 == 0; N % 16 == 0; M in 1..128;
+ *    device pointers 16-byte aligned.
+ *
+ * Packed weight layout ("tile layout"; this library's own, the paper gives none)
+ *  - A tile holds the codes of 16 output columns x 128 inputs.  Tile (nt, kb),
+ *    nt = n / 16, kb = k / 128, starts at byte 256 * bits * (nt * (K/128) + kb), so
+ *    the whole buffer is N * K * bits / 8 bytes (subspec_qpack_bytes).
+ *  - A tile is 64 slices of 4*bits bytes.  Slice L (0..63) belongs to column
+ *    n = 16*nt + L % 16 and holds 32 codes: for step j (0..3) and element e (0..7)
+ *    the code of k = 128*kb + 32*j + 8*(L/16) + e.
+ *  - The 32 codes form 16 pairs p = 4*j + e/2.  Within a slice read as
+ *    little-endian 32-bit words, a pair's even-e code sits at bit offset o of a
+ *    word and its odd-e code at offset o + 16 of the same word:
+ *      bits 4: word p/4, o = 4*(p%4)
+ *      bits 2: word p/8, o = 2*(p%8)
+ *      bits 3: pairs 0..14: word p/5, o = 3*(p%5);  pair 15: bit c (c = 0,1,2) of
+ *              the even code is bit 15 of word c, of the odd code bit 31 of word c.
+ *    One 64-lane wavefront reading one slice per lane reads a whole tile as one
+ *    contiguous run, and every pair unpacks with a shift and one and-or into two
+ *    16-bit fields.
+ *  - Scales and zeros are fp16 arrays [K/group][N], row-major (s[g][n] at g*N + n).
+ */
+#ifndef SUBSPEC_H_
+#define SUBSPEC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum subspec_status {
+  SUBSPEC_OK = 0,
+  SUBSPEC_EINVAL = -1,       /* bad argument (null/misaligned pointer, bad size) */
+  SUBSPEC_EUNSUPPORTED = -2, /* well-formed but outside bits/group/M/N/K support */
+  SUBSPEC_EHIP = -3,         /* a HIP runtime call or kernel launch failed        */
+  SUBSPEC_ECAPTURE = -4      /* the call needs to grow its workspace while the
+                                stream is being captured; call subspec_reserve()
+                                before capturing                                  */
+};
+
+/* Kernel paths (subspec_plan.path, subspec_qlinear_path's `path`). */
+enum subspec_path {
+  SUBSPEC_PATH_AUTO = 0, /* let subspec_qlinear_plan choose                        */
+  SUBSPEC_PATH_GEMV = 1, /* VALU dot products, lanes split K, DPP/permlane and LDS
+                            split-K reductions; M <= 8                            */
+  SUBSPEC_PATH_MFMA = 2  /* bf16 matrix cores on unpacked code tiles; any M        */
+};
+
+/* Launch configuration chosen for one qlinear call (host-side description). */
+typedef struct subspec_plan {
+  int path;            /* SUBSPEC_PATH_GEMV or SUBSPEC_PATH_MFMA                  */
+  int rows;            /* rows computed per workgroup (M rounded up)              */
+  int tiles_per_wave;  /* 16-column tiles each wavefront owns                     */
+  int chunk_blocks;    /* 128-k blocks staged in LDS per step                     */
+  int col_groups;      /* workgroups along N                                      */
+  int splits;          /* workgroups along K (split-K); 1 = no partial results    */
+  int blocks_per_split;/* 128-k blocks per split                                  */
+  int grid;            /* total workgroups = col_groups * splits                  */
+  size_t workspace_bytes; /* device scratch needed (fp32 partials + counters)    */
+} subspec_plan;
+
+/* Bytes of the packed code buffer for an N x K projection.  0 on bad arguments. */
+size_t subspec_qpack_bytes(int bits, int N, int K);
+
+/* Quantize fp32 weights per group with the min/max asymmetric rule (the paper's
+ * data-free substitute construction, Sec. 4.1; the rule itself is this library's
+ * reading, the paper names HQQ without its algorithm):
+ *   s = (wmax - wmin) / (2^bits - 1) in float64;  s16 = fp16(s) nearest-even;
+ *   z16 = fp16(-wmin / s16);  q = clamp(rint(w / s16 + z16), 0, 2^bits - 1),
+ * every step in float64 (ties to even); a group with wmax == wmin or s16 == 0 gets
+ * s16 = 1, z16 = fp16(-wmin), q = 0.
+ *   w      device fp32 [N][K] row-major (read only)
+ *   codes  device uint8 [N][K] row-major, one code per byte (written)
+ *   scales, zeros  device fp16 [K/group][N] (written)
+ * Needs K % group == 0 and N >= 1; K need not be a multiple of 128 here. */
+int subspec_quantize(const float* w, int bits, int group, int N, int K,
+                     uint8_t* codes, uint16_t* scales, uint16_t* zeros,
+                     hipStream_t stream);
+
+/* Pack one-byte codes (device uint8 [N][K], each < 2^bits) into the tile layout
+ * above (device, subspec_qpack_bytes() bytes, written).  Codes with bits above
+ * `bits` set are masked off. */
+int subspec_qpack(const uint8_t* codes, int bits, int N, int K, void* qweight,
+                  hipStream_t stream);
+
+/* Same as subspec_qpack on host memory, synchronous, no GPU needed. */
+int subspec_qpack_host(const uint8_t* codes, int bits, int N, int K, void* qweight);
+
+/* The substitute layer (Sec. 4.1): y = x * dequant(qweight, scales, zeros)^T.
+ *   x        device bf16 [M][K] row-major
+ *   qweight  device, tile layout, subspec_qpack_bytes(bits, N, K) bytes
+ *   scales   device fp16 [K/group][N]
+ *   zeros    device fp16 [K/group][N]
+ *   y        device bf16 [M][N] row-major, fully overwritten
+ * x and y must not overlap each other or the weights.  Uses the library's
+ * per-device workspace when the plan splits K (see subspec_reserve); calls that
+ * overlap in time on one device (different streams) must not share it, so
+ * serialise them. */
+int subspec_qlinear(const void* x, const void* qweight, const void* scales,
+                    const void* zeros, int bits, int group, int M, int N, int K,
+                    void* y, hipStream_t stream);
+
+/* subspec_qlinear with an explicit kernel path (SUBSPEC_PATH_*): for tests and
+ * A/B measurements.  SUBSPEC_PATH_GEMV requires M <= 8. */
+int subspec_qlinear_path(const void* x, const void* qweight, const void* scales,
+                         const void* zeros, int bits, int group, int M, int N, int K,
+                         void* y, int path, hipStream_t stream);
+
+/* Host only, no GPU needed: validate the shape and fill *plan with the launch
+ * configuration subspec_qlinear_path would use for `path` (AUTO allowed). */
+int subspec_qlinear_plan(int M, int N, int K, int bits, int group, int path,
+                         subspec_plan* plan);
+
+/* Materialise the dequantized weights from the packed layout (the same unpacking
+ * code the qlinear kernels use):
+ *   w_f32[n][k]  = fma(q, s, -s*z) in fp32, which equals s*(q - z) rounded once
+ *                  (s*z of two fp16 values is exact in fp32);
+ *   w_bf16[n][k] = that fp32 value rounded to bf16, nearest-even.
+ * Either output pointer may be null.  Outputs are device [N][K] row-major. */
+int subspec_qdequant(const void* qweight, const void* scales, const void* zeros,
+                     int bits, int group, int N, int K, float* w_f32,
+                     uint16_t* w_bf16, hipStream_t stream);
+
+/* Grow the calling device's workspace to at least `bytes` now (synchronous, may
+ * call hipMalloc), so that later calls, e.g. under stream capture, need not. */
+int subspec_reserve(size_t bytes);
+
+/* Description of the last failure on this thread ("" if none). */
+const char* subspec_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SUBSPEC_H_ */

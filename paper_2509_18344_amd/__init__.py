@@ -1,0 +1,25 @@
+"""MI355X (gfx950) low-bit substitute layers of SubSpec (Sec. 4.1).
+
+The compute path is the native library ``libsubspec.so`` (hand-written HIP,
+C ABI in ``include/subspec.h``); this package only marshals arguments to it.
+Importing works without a GPU; calling a device entry point needs the library
+built for gfx950 and fails loudly when it is missing.
+"""
+from ._binding import (  # noqa: F401
+    SUBSPEC_PATH_AUTO,
+    SUBSPEC_PATH_GEMV,
+    SUBSPEC_PATH_MFMA,
+    SubspecError,
+    library_path,
+    load_library,
+    subspec_last_error,
+    subspec_qdequant,
+    subspec_qlinear,
+    subspec_qlinear_path,
+    subspec_qlinear_plan,
+    subspec_qpack,
+    subspec_qpack_bytes,
+    subspec_qpack_host,
+    subspec_quantize,
+    subspec_reserve,
+)

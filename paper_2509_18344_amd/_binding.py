@@ -1,0 +1,150 @@
+"""ctypes binding of libsubspec.so: one Python function per C entry point, with the
+same name and argument order.  Tensors are passed as their data pointers; a
+``stream`` of None means torch's current stream on the current device."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_NAME = "libsubspec.so"
+
+SUBSPEC_PATH_AUTO = 0
+SUBSPEC_PATH_GEMV = 1
+SUBSPEC_PATH_MFMA = 2
+
+_STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EHIP", -4: "ECAPTURE"}
+
+
+class SubspecError(RuntimeError):
+    def __init__(self, fn: str, status: int, message: str):
+        super().__init__(f"{fn} failed with {_STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class _Plan(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int), ("rows", ctypes.c_int), ("tiles_per_wave", ctypes.c_int),
+                ("chunk_blocks", ctypes.c_int), ("col_groups", ctypes.c_int),
+                ("splits", ctypes.c_int), ("blocks_per_split", ctypes.c_int),
+                ("grid", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, _LIB_NAME)
+
+
+def load_library():
+    """Load libsubspec.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
+                           "(or python -m paper_2509_18344_amd.build)")
+    lib = ctypes.CDLL(path)
+    P, I, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    sig = {
+        "subspec_qpack_bytes": (S, [I, I, I]),
+        "subspec_quantize": (I, [P, I, I, I, I, P, P, P, P]),
+        "subspec_qpack": (I, [P, I, I, I, P, P]),
+        "subspec_qpack_host": (I, [P, I, I, I, P]),
+        "subspec_qlinear": (I, [P, P, P, P, I, I, I, I, I, P, P]),
+        "subspec_qlinear_path": (I, [P, P, P, P, I, I, I, I, I, P, I, P]),
+        "subspec_qlinear_plan": (I, [I, I, I, I, I, I, ctypes.POINTER(_Plan)]),
+        "subspec_qdequant": (I, [P, P, P, I, I, I, I, P, P, P]),
+        "subspec_reserve": (I, [S]),
+        "subspec_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    """Data pointer of a torch tensor / numpy array, or an int address, or None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if hasattr(t, "data_ptr"):
+        return t.data_ptr()
+    if hasattr(t, "ctypes"):
+        return t.ctypes.data
+    raise TypeError(f"cannot take the address of {type(t)}")
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(fn: str, status: int) -> int:
+    if status != 0:
+        raise SubspecError(fn, status, subspec_last_error())
+    return status
+
+
+def subspec_last_error() -> str:
+    return load_library().subspec_last_error().decode()
+
+
+def subspec_qpack_bytes(bits: int, N: int, K: int) -> int:
+    return int(load_library().subspec_qpack_bytes(bits, N, K))
+
+
+def subspec_quantize(w, bits, group, N, K, codes, scales, zeros, stream=None) -> int:
+    return _check("subspec_quantize", load_library().subspec_quantize(
+        _ptr(w), bits, group, N, K, _ptr(codes), _ptr(scales), _ptr(zeros), _stream(stream)))
+
+
+def subspec_qpack(codes, bits, N, K, qweight, stream=None) -> int:
+    return _check("subspec_qpack", load_library().subspec_qpack(
+        _ptr(codes), bits, N, K, _ptr(qweight), _stream(stream)))
+
+
+def subspec_qpack_host(codes, bits, N, K, qweight) -> int:
+    return _check("subspec_qpack_host", load_library().subspec_qpack_host(
+        _ptr(codes), bits, N, K, _ptr(qweight)))
+
+
+def subspec_qlinear(x, qweight, scales, zeros, bits, group, M, N, K, y, stream=None) -> int:
+    return _check("subspec_qlinear", load_library().subspec_qlinear(
+        _ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), bits, group, M, N, K, _ptr(y),
+        _stream(stream)))
+
+
+def subspec_qlinear_path(x, qweight, scales, zeros, bits, group, M, N, K, y, path,
+                         stream=None) -> int:
+    return _check("subspec_qlinear_path", load_library().subspec_qlinear_path(
+        _ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), bits, group, M, N, K, _ptr(y), path,
+        _stream(stream)))
+
+
+def subspec_qlinear_plan(M, N, K, bits, group, path=SUBSPEC_PATH_AUTO) -> dict:
+    p = _Plan()
+    _check("subspec_qlinear_plan", load_library().subspec_qlinear_plan(
+        M, N, K, bits, group, path, ctypes.byref(p)))
+    return {name: getattr(p, name) for name, _ in _Plan._fields_}
+
+
+def subspec_qdequant(qweight, scales, zeros, bits, group, N, K, w_f32, w_bf16,
+                     stream=None) -> int:
+    return _check("subspec_qdequant", load_library().subspec_qdequant(
+        _ptr(qweight), _ptr(scales), _ptr(zeros), bits, group, N, K, _ptr(w_f32), _ptr(w_bf16),
+        _stream(stream)))
+
+
+def subspec_reserve(nbytes: int) -> int:
+    return _check("subspec_reserve", load_library().subspec_reserve(nbytes))

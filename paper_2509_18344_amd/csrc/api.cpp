@@ -1,0 +1,362 @@
+// C ABI of the library (include/subspec.h): argument validation, launch planning,
+// the per-device split-K workspace, the host packer and error reporting.
+#include "subspec.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(SUBSPEC_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_bits_group(int bits, int group) {
+  if (bits < 2 || bits > 4) return fail(SUBSPEC_EUNSUPPORTED, "bits=%d: must be 2, 3 or 4", bits);
+  if (group != 64 && group != 128)
+    return fail(SUBSPEC_EUNSUPPORTED, "group=%d: must be 64 or 128", group);
+  return SUBSPEC_OK;
+}
+
+int check_tiles(int N, int K) {
+  if (N <= 0 || K <= 0) return fail(SUBSPEC_EINVAL, "N=%d, K=%d: must be positive", N, K);
+  if (N % subspec::kTileN) return fail(SUBSPEC_EUNSUPPORTED, "N=%d: must be a multiple of 16", N);
+  if (K % subspec::kTileK) return fail(SUBSPEC_EUNSUPPORTED, "K=%d: must be a multiple of 128", K);
+  if (static_cast<long long>(N) * K > (1ll << 40))
+    return fail(SUBSPEC_EUNSUPPORTED, "N*K=%lld too large", static_cast<long long>(N) * K);
+  return SUBSPEC_OK;
+}
+
+constexpr int kMaxRows = 128;
+constexpr int kGemvMaxRows = 8;
+
+// --- launch planning --------------------------------------------------------
+
+struct Tuning {
+  int gemv_max_m = kGemvMaxRows;  // largest M the automatic plan sends to the GEMV path
+  int target_blocks = 1024;       // workgroups the split-K choice aims for
+  int gemv_nt = 1;
+  int mfma_nt = 2;
+};
+
+// Optional overrides for measurement sweeps: SUBSPEC_TUNE="gemv_max_m=4,target=512,...".
+const Tuning& tuning() {
+  static Tuning t = [] {
+    Tuning r;
+    const char* env = std::getenv("SUBSPEC_TUNE");
+    if (!env) return r;
+    std::string s(env);
+    size_t pos = 0;
+    while (pos < s.size()) {
+      size_t end = s.find(',', pos);
+      if (end == std::string::npos) end = s.size();
+      std::string kv = s.substr(pos, end - pos);
+      size_t eq = kv.find('=');
+      if (eq != std::string::npos) {
+        const std::string k = kv.substr(0, eq);
+        const int v = std::atoi(kv.c_str() + eq + 1);
+        if (k == "gemv_max_m") r.gemv_max_m = v;
+        else if (k == "target") r.target_blocks = v;
+        else if (k == "gemv_nt") r.gemv_nt = v;
+        else if (k == "mfma_nt") r.mfma_nt = v;
+      }
+      pos = end + 1;
+    }
+    return r;
+  }();
+  return t;
+}
+
+int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* p,
+              subspec::KernelChoice* kc) {
+  int rc = check_bits_group(bits, group);
+  if (rc) return rc;
+  rc = check_tiles(N, K);
+  if (rc) return rc;
+  if (M < 1 || M > kMaxRows) return fail(SUBSPEC_EUNSUPPORTED, "M=%d: must be in 1..%d", M, kMaxRows);
+  const Tuning& tu = tuning();
+  if (path == SUBSPEC_PATH_AUTO) path = (M <= tu.gemv_max_m) ? SUBSPEC_PATH_GEMV : SUBSPEC_PATH_MFMA;
+  subspec::KernelChoice c{};
+  if (path == SUBSPEC_PATH_GEMV) {
+    if (M > kGemvMaxRows) return fail(SUBSPEC_EUNSUPPORTED, "GEMV path needs M <= 8 (M=%d)", M);
+    c.path = 1;
+    c.rows = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 8;
+    c.nt = tu.gemv_nt;
+    c.chunk = 4;
+  } else if (path == SUBSPEC_PATH_MFMA) {
+    c.path = 2;
+    const int mt = M <= 16 ? 1 : M <= 32 ? 2 : M <= 64 ? 4 : 8;
+    c.rows = 16 * mt;
+    c.nt = tu.mfma_nt;
+    c.chunk = mt == 1 ? 4 : mt == 8 ? 1 : 2;
+  } else {
+    return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
+  }
+  if (!subspec::qlinear_variant_exists(c, bits, group))
+    return fail(SUBSPEC_EUNSUPPORTED, "no kernel for path=%d rows=%d nt=%d chunk=%d bits=%d group=%d",
+                c.path, c.rows, c.nt, c.chunk, bits, group);
+  const int KB = K / subspec::kTileK;
+  const int cols_per_group = subspec::kWavesPerBlock * c.nt * subspec::kTileN;
+  const int col_groups = (N + cols_per_group - 1) / cols_per_group;
+  const int chunks = (KB + c.chunk - 1) / c.chunk;
+  int splits = (tu.target_blocks + col_groups - 1) / col_groups;
+  if (splits < 1) splits = 1;
+  if (splits > chunks) splits = chunks;
+  int chunks_per_split = (chunks + splits - 1) / splits;
+  const int blocks_per_split = chunks_per_split * c.chunk;
+  splits = (KB + blocks_per_split - 1) / blocks_per_split;
+  p->path = path;
+  p->rows = c.rows;
+  p->tiles_per_wave = c.nt;
+  p->chunk_blocks = c.chunk;
+  p->col_groups = col_groups;
+  p->splits = splits;
+  p->blocks_per_split = blocks_per_split;
+  p->grid = col_groups * splits;
+  p->workspace_bytes = 0;
+  if (splits > 1) {
+    const size_t counters = (static_cast<size_t>(col_groups) * 4 + 255) / 256 * 256;
+    p->workspace_bytes = counters + static_cast<size_t>(splits) * M * N * sizeof(float);
+  }
+  if (kc) *kc = c;
+  return SUBSPEC_OK;
+}
+
+// --- per-device workspace -----------------------------------------------------
+
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_ws_mutex;
+std::vector<Workspace> g_ws;
+
+int current_device(int* dev) {
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  return SUBSPEC_OK;
+}
+
+// Returns the device's workspace, grown to `bytes` if needed.  Growth allocates
+// (synchronously) and zero-fills, so it is refused while `st` is being captured.
+int get_workspace(size_t bytes, hipStream_t st, void** out) {
+  int dev = 0;
+  int rc = current_device(&dev);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  if (static_cast<int>(g_ws.size()) <= dev) g_ws.resize(dev + 1);
+  Workspace& w = g_ws[dev];
+  if (w.bytes >= bytes) {
+    *out = w.ptr;
+    return SUBSPEC_OK;
+  }
+  if (st != nullptr) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(st, &cs);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+    if (cs != hipStreamCaptureStatusNone)
+      return fail(SUBSPEC_ECAPTURE, "workspace must grow to %zu bytes during stream capture; call "
+                  "subspec_reserve() first", bytes);
+  }
+  size_t nb = bytes < (size_t(1) << 20) ? (size_t(1) << 20) : bytes;
+  nb = (nb + 0xFFFFF) & ~size_t(0xFFFFF);
+  hipError_t e = hipDeviceSynchronize();  // the old buffer may still be in use
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  if (w.ptr) {
+    e = hipFree(w.ptr);
+    if (e != hipSuccess) return hip_fail(e, "hipFree(workspace)");
+    w.ptr = nullptr;
+    w.bytes = 0;
+  }
+  void* p = nullptr;
+  e = hipMalloc(&p, nb);
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
+  e = hipMemset(p, 0, nb);
+  if (e != hipSuccess) {
+    hipFree(p);
+    return hip_fail(e, "hipMemset(workspace)");
+  }
+  w.ptr = p;
+  w.bytes = nb;
+  *out = p;
+  return SUBSPEC_OK;
+}
+
+// --- host packer (the same layout as the device packer) ----------------------
+
+template <int BITS>
+void pack_slice_host(const uint32_t c[32], uint32_t* out) {
+  const uint32_t mask = (1u << BITS) - 1;
+  for (int w = 0; w < BITS; ++w) out[w] = 0;
+  for (int p = 0; p < 16; ++p) {
+    const int j = p / 4, i = p % 4;
+    const uint32_t ev = c[8 * j + 2 * i] & mask, od = c[8 * j + 2 * i + 1] & mask;
+    if (BITS == 4) {
+      out[p / 4] |= (ev << (4 * (p % 4))) | (od << (16 + 4 * (p % 4)));
+    } else if (BITS == 2) {
+      out[p / 8] |= (ev << (2 * (p % 8))) | (od << (16 + 2 * (p % 8)));
+    } else if (p < 15) {
+      out[p / 5] |= (ev << (3 * (p % 5))) | (od << (16 + 3 * (p % 5)));
+    } else {
+      for (int b = 0; b < 3; ++b) out[b] |= (((ev >> b) & 1u) << 15) | (((od >> b) & 1u) << 31);
+    }
+  }
+}
+
+template <int BITS>
+void pack_host(const uint8_t* codes, int N, int K, uint8_t* out) {
+  const int KB = K / subspec::kTileK;
+  uint32_t c[32], words[BITS];
+  for (long long nt = 0; nt < N / subspec::kTileN; ++nt)
+    for (int kb = 0; kb < KB; ++kb)
+      for (int L = 0; L < 64; ++L) {
+        const long long n = nt * subspec::kTileN + L % 16;
+        const uint8_t* row = codes + n * K + kb * subspec::kTileK + 8 * (L / 16);
+        for (int j = 0; j < 4; ++j)
+          for (int e = 0; e < 8; ++e) c[8 * j + e] = row[32 * j + e];
+        pack_slice_host<BITS>(c, words);
+        uint8_t* dst = out + ((nt * KB + kb) * 64 + L) * (4 * BITS);
+        std::memcpy(dst, words, 4 * BITS);  // little-endian host
+      }
+}
+
+int qlinear_impl(const void* x, const void* qweight, const void* scales, const void* zeros,
+                 int bits, int group, int M, int N, int K, void* y, int path, hipStream_t st) {
+  subspec_plan p;
+  subspec::KernelChoice kc;
+  int rc = make_plan(M, N, K, bits, group, path, &p, &kc);
+  if (rc) return rc;
+  if (!x || !qweight || !scales || !zeros || !y) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (!aligned16(x) || !aligned16(qweight) || !aligned16(scales) || !aligned16(zeros) || !aligned16(y))
+    return fail(SUBSPEC_EINVAL, "device pointers must be 16-byte aligned");
+  subspec::QArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.qw = static_cast<const uint8_t*>(qweight);
+  a.sc = static_cast<const uint16_t*>(scales);
+  a.zr = static_cast<const uint16_t*>(zeros);
+  a.y = static_cast<uint16_t*>(y);
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.KB = K / subspec::kTileK;
+  a.n_tiles = N / subspec::kTileN;
+  a.splits = p.splits;
+  a.blocks_per_split = p.blocks_per_split;
+  if (p.splits > 1) {
+    void* ws = nullptr;
+    rc = get_workspace(p.workspace_bytes, st, &ws);
+    if (rc) return rc;
+    const size_t counters = (static_cast<size_t>(p.col_groups) * 4 + 255) / 256 * 256;
+    a.counters = static_cast<unsigned*>(ws);
+    a.ws = reinterpret_cast<float*>(static_cast<char*>(ws) + counters);
+  }
+  hipError_t e = subspec::launch_qlinear(kc, bits, group, a, p.grid, st);
+  if (e != hipSuccess) return hip_fail(e, "qlinear launch");
+  return SUBSPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t subspec_qpack_bytes(int bits, int N, int K) {
+  if (bits < 2 || bits > 4 || N <= 0 || K <= 0 || N % subspec::kTileN || K % subspec::kTileK) return 0;
+  return static_cast<size_t>(N) * K / 8 * bits;
+}
+
+int subspec_quantize(const float* w, int bits, int group, int N, int K, uint8_t* codes,
+                     uint16_t* scales, uint16_t* zeros, hipStream_t stream) {
+  int rc = check_bits_group(bits, group);
+  if (rc) return rc;
+  if (N <= 0 || K <= 0 || K % group) return fail(SUBSPEC_EINVAL, "N=%d K=%d group=%d: bad shape", N, K, group);
+  if (!w || !codes || !scales || !zeros) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (!aligned16(w) || !aligned16(codes) || !aligned16(scales) || !aligned16(zeros))
+    return fail(SUBSPEC_EINVAL, "device pointers must be 16-byte aligned");
+  hipError_t e = subspec::launch_quantize(w, bits, group, N, K, codes, scales, zeros, stream);
+  if (e != hipSuccess) return hip_fail(e, "quantize launch");
+  return SUBSPEC_OK;
+}
+
+int subspec_qpack(const uint8_t* codes, int bits, int N, int K, void* qweight, hipStream_t stream) {
+  if (bits < 2 || bits > 4) return fail(SUBSPEC_EUNSUPPORTED, "bits=%d: must be 2, 3 or 4", bits);
+  int rc = check_tiles(N, K);
+  if (rc) return rc;
+  if (!codes || !qweight) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (!aligned16(codes) || !aligned16(qweight)) return fail(SUBSPEC_EINVAL, "device pointers must be 16-byte aligned");
+  hipError_t e = subspec::launch_qpack(codes, bits, N, K, qweight, stream);
+  if (e != hipSuccess) return hip_fail(e, "qpack launch");
+  return SUBSPEC_OK;
+}
+
+int subspec_qpack_host(const uint8_t* codes, int bits, int N, int K, void* qweight) {
+  if (bits < 2 || bits > 4) return fail(SUBSPEC_EUNSUPPORTED, "bits=%d: must be 2, 3 or 4", bits);
+  int rc = check_tiles(N, K);
+  if (rc) return rc;
+  if (!codes || !qweight) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  uint8_t* out = static_cast<uint8_t*>(qweight);
+  if (bits == 4) pack_host<4>(codes, N, K, out);
+  else if (bits == 3) pack_host<3>(codes, N, K, out);
+  else pack_host<2>(codes, N, K, out);
+  return SUBSPEC_OK;
+}
+
+int subspec_qlinear(const void* x, const void* qweight, const void* scales, const void* zeros,
+                    int bits, int group, int M, int N, int K, void* y, hipStream_t stream) {
+  return qlinear_impl(x, qweight, scales, zeros, bits, group, M, N, K, y, SUBSPEC_PATH_AUTO, stream);
+}
+
+int subspec_qlinear_path(const void* x, const void* qweight, const void* scales, const void* zeros,
+                         int bits, int group, int M, int N, int K, void* y, int path,
+                         hipStream_t stream) {
+  return qlinear_impl(x, qweight, scales, zeros, bits, group, M, N, K, y, path, stream);
+}
+
+int subspec_qlinear_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* plan) {
+  if (!plan) return fail(SUBSPEC_EINVAL, "null plan pointer");
+  return make_plan(M, N, K, bits, group, path, plan, nullptr);
+}
+
+int subspec_qdequant(const void* qweight, const void* scales, const void* zeros, int bits,
+                     int group, int N, int K, float* w_f32, uint16_t* w_bf16, hipStream_t stream) {
+  int rc = check_bits_group(bits, group);
+  if (rc) return rc;
+  rc = check_tiles(N, K);
+  if (rc) return rc;
+  if (!qweight || !scales || !zeros) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (!w_f32 && !w_bf16) return SUBSPEC_OK;
+  hipError_t e = subspec::launch_qdequant(qweight, scales, zeros, bits, group, N, K, w_f32, w_bf16, stream);
+  if (e != hipSuccess) return hip_fail(e, "qdequant launch");
+  return SUBSPEC_OK;
+}
+
+int subspec_reserve(size_t bytes) {
+  void* p = nullptr;
+  return get_workspace(bytes, nullptr, &p);
+}
+
+const char* subspec_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

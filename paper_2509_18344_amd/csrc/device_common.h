@@ -1,0 +1,86 @@
+// Device-side building blocks shared by every kernel of the library: slice loads
+// and code unpacking for the tile layout declared in include/subspec.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.h"
+
+namespace subspec {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+
+// Bias added to every unpacked code: the 16-bit field 0x4300 | q is the bf16 value
+// 128 + q exactly (exponent 2^7, seven mantissa bits of weight 1), for q < 128.
+constexpr uint32_t kPairBias = 0x43004300u;
+constexpr float kCodeBias = 128.0f;
+
+// Raw words of one slice (4*BITS bytes, one per lane of a tile).
+template <int BITS>
+struct Slice {
+  uint32_t w[BITS];
+};
+
+template <int BITS>
+__device__ __forceinline__ Slice<BITS> load_slice(const uint8_t* __restrict__ p) {
+  Slice<BITS> s;
+  if constexpr (BITS == 4) {
+    uint4 v = *reinterpret_cast<const uint4*>(p);
+    s.w[0] = v.x; s.w[1] = v.y; s.w[2] = v.z; s.w[3] = v.w;
+  } else if constexpr (BITS == 2) {
+    uint2 v = *reinterpret_cast<const uint2*>(p);
+    s.w[0] = v.x; s.w[1] = v.y;
+  } else {
+    struct __attribute__((packed, aligned(4))) U3 { uint32_t a, b, c; };
+    U3 v = *reinterpret_cast<const U3*>(p);
+    s.w[0] = v.a; s.w[1] = v.b; s.w[2] = v.c;
+  }
+  return s;
+}
+
+// Unpack a slice into its 16 pairs.  pr[p] holds (0x4300 | q_even) in the low and
+// (0x4300 | q_odd) in the high 16 bits, i.e. two bf16 values 128 + q; pair p covers
+// elements e = 2*(p%4), 2*(p%4)+1 of step p/4.
+template <int BITS>
+__device__ __forceinline__ void unpack_pairs(const Slice<BITS>& s, uint32_t pr[16]) {
+  if constexpr (BITS == 4) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t d = s.w[j];
+      pr[4 * j + 0] = (d & 0x000F000Fu) | kPairBias;
+      pr[4 * j + 1] = ((d >> 4) & 0x000F000Fu) | kPairBias;
+      pr[4 * j + 2] = ((d >> 8) & 0x000F000Fu) | kPairBias;
+      pr[4 * j + 3] = ((d >> 12) & 0x000F000Fu) | kPairBias;
+    }
+  } else if constexpr (BITS == 2) {
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+      const uint32_t d = s.w[w];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) pr[8 * w + t] = ((d >> (2 * t)) & 0x00030003u) | kPairBias;
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < 3; ++w) {
+      const uint32_t d = s.w[w];
+#pragma unroll
+      for (int t = 0; t < 5; ++t) pr[5 * w + t] = ((d >> (3 * t)) & 0x00070007u) | kPairBias;
+    }
+    pr[15] = ((s.w[0] >> 15) & 0x00010001u) | ((s.w[1] >> 14) & 0x00020002u) |
+             ((s.w[2] >> 13) & 0x00040004u) | kPairBias;
+  }
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, h));
+}
+
+// fp32 -> bf16, round to nearest even (hardware conversion on gfx950).
+__device__ __forceinline__ uint16_t float_to_bf16_bits(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+}  // namespace subspec

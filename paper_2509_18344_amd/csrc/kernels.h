@@ -1,0 +1,51 @@
+// Host-visible launchers of the library's kernels (internal; the public ABI is
+// include/subspec.h).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace subspec {
+
+constexpr int kTileN = 16;    // output columns per tile
+constexpr int kTileK = 128;   // inputs per tile (one "block")
+constexpr int kWave = 64;
+
+// Everything a qlinear kernel needs; filled by the host dispatcher from a plan.
+struct QArgs {
+  const uint16_t* x;      // bf16 [M][K]
+  const uint8_t* qw;      // tile layout
+  const uint16_t* sc;     // fp16 [K/group][N]
+  const uint16_t* zr;     // fp16 [K/group][N]
+  uint16_t* y;            // bf16 [M][N]
+  float* ws;              // fp32 [splits][M][N] partial sums (splits > 1)
+  unsigned* counters;     // [col_groups] arrival counters, zero between calls
+  int M, N, K;
+  int KB;                 // K / 128
+  int n_tiles;            // N / 16
+  int splits;
+  int blocks_per_split;
+};
+
+struct KernelChoice {
+  int path;    // 1 = GEMV, 2 = MFMA
+  int rows;    // GEMV: 1, 2, 4, 8; MFMA: 16 * m-tiles
+  int nt;      // tiles per wavefront
+  int chunk;   // 128-k blocks per LDS stage
+};
+
+hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a,
+                          int grid, hipStream_t st);
+bool qlinear_variant_exists(const KernelChoice& kc, int bits, int group);
+
+hipError_t launch_quantize(const float* w, int bits, int group, int N, int K, uint8_t* codes,
+                           uint16_t* sc, uint16_t* zr, hipStream_t st);
+hipError_t launch_qpack(const uint8_t* codes, int bits, int N, int K, void* qw, hipStream_t st);
+hipError_t launch_qdequant(const void* qw, const void* sc, const void* zr, int bits, int group,
+                           int N, int K, float* wf, uint16_t* wb, hipStream_t st);
+
+constexpr int kWavesPerBlock = 4;
+constexpr int kThreadsPerBlock = 256;
+
+}  // namespace subspec

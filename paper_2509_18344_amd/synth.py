@@ -1,0 +1,59 @@
+"""Seeded synthetic inputs shaped like the paper's draft-model workloads.
+
+Only random numbers and their placement live here -- no quantization, packing or
+matmul arithmetic -- so both the HIP path and the CPU oracle can take the very
+same inputs.  Weights are N(0, 0.02) float32; activations are N(0, 1) rounded to
+bfloat16 (round-to-nearest-even), optionally with a fraction of input channels
+scaled by 20 before rounding (outlier channels).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def seed_of(*keys: int) -> int:
+    """A 63-bit seed derived from a tuple of non-negative integers."""
+    ss = np.random.SeedSequence([int(k) for k in keys])
+    return int(ss.generate_state(1, dtype=np.uint64)[0] & np.uint64(0x7FFF_FFFF_FFFF_FFFF))
+
+
+def weights_np(N: int, K: int, *keys: int, std: float = 0.02) -> np.ndarray:
+    """float32 [N][K] ~ N(0, std^2), generated on the host."""
+    rng = np.random.default_rng(np.random.SeedSequence([int(k) for k in keys]))
+    return (rng.standard_normal((N, K), dtype=np.float32) * np.float32(std)).astype(np.float32)
+
+
+def weights_torch(N: int, K: int, *keys: int, device="cuda", std: float = 0.02):
+    """float32 [N][K] ~ N(0, std^2), generated directly on ``device`` by torch's
+    seeded generator (used for the multi-GB stacks)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed_of(*keys))
+    w = torch.randn((N, K), generator=g, device=device, dtype=torch.float32)
+    return w.mul_(std)
+
+
+def outlier_channels(K: int, frac: float, *keys: int) -> np.ndarray:
+    """round(frac*K) distinct input channels, chosen by a seeded RNG."""
+    n = int(round(frac * K))
+    rng = np.random.default_rng(np.random.SeedSequence([int(k) for k in keys] + [7]))
+    return np.sort(rng.choice(K, size=n, replace=False))
+
+
+def activations(M: int, K: int, *keys: int, outlier_frac: float = 0.0,
+                outlier_scale: float = 20.0):
+    """bfloat16 torch tensor [M][K] (CPU): N(0, 1) float32, outlier channels
+    multiplied by ``outlier_scale`` in float32, then rounded to bf16."""
+    import torch
+    rng = np.random.default_rng(np.random.SeedSequence([int(k) for k in keys]))
+    x = rng.standard_normal((M, K), dtype=np.float32)
+    if outlier_frac > 0:
+        ch = outlier_channels(K, outlier_frac, *keys)
+        x[:, ch] *= np.float32(outlier_scale)
+    return torch.from_numpy(x).to(torch.bfloat16)
+
+
+def bf16_bits(t) -> np.ndarray:
+    """uint16 bit patterns of a (CPU) bfloat16 tensor."""
+    import torch
+    return t.contiguous().view(torch.int16).numpy().view(np.uint16)

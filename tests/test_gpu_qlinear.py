@@ -1,0 +1,144 @@
+"""GPU parity of the HIP path against the fp64 CPU oracle, through the C ABI.
+
+Integer/bit work (quantizer codes, fp16 scale/zero, packing, dequantization) must be
+bit-exact; layer outputs must satisfy |y - y_ref| <= 1e-3 + 1e-2 |y_ref| element-wise,
+with y_ref computed by the oracle on the exact dequantized weights."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2509_18344_amd as ss
+from paper_2509_18344_amd import synth
+
+from helpers import assert_close, bf16_to_f64, device_projection, run_qlinear
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _w(N, K, *keys):
+    return synth.weights_np(N, K, *keys)
+
+
+# ------------------------------------------------------------------ preparation
+
+@pytest.mark.parametrize("bits,group", [(4, 64), (4, 128), (3, 128), (3, 64), (2, 64), (2, 128)])
+def test_quantize_bit_exact(bits, group):
+    N, K = 80, 768
+    w = _w(N, K, 100, bits, group)
+    # a few adversarial groups: constant, all positive, all negative, tiny range
+    w[0, :group] = 0.25
+    w[1, :group] = np.linspace(0.5, 2.0, group)
+    w[2, :group] = np.linspace(-3.0, -1.0, group)
+    w[3, :group] = np.tile((np.arange(group // 4) - 5.0) * 2.0 ** -22, 4)[:group]
+    p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+    q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+    torch.cuda.synchronize()
+    assert np.array_equal(p["codes"].cpu().numpy(), q)
+    assert np.array_equal(p["scales"].cpu().numpy().view(np.uint16), s16.view(np.uint16))
+    assert np.array_equal(p["zeros"].cpu().numpy().view(np.uint16), z16.view(np.uint16))
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_device_pack_matches_layout(bits):
+    N, K = 48, 640
+    rng = np.random.default_rng(bits)
+    codes = rng.integers(0, 2 ** bits, (N, K)).astype(np.uint8)
+    qw = torch.empty(ss.subspec_qpack_bytes(bits, N, K), dtype=torch.uint8, device=DEV)
+    ss.subspec_qpack(torch.from_numpy(codes).to(DEV), bits, N, K, qw)
+    torch.cuda.synchronize()
+    assert np.array_equal(oracle.unpack(qw.cpu().numpy(), bits, N, K), codes)
+
+
+@pytest.mark.parametrize("bits,group", [(4, 64), (4, 128), (3, 128), (2, 64)])
+def test_dequant_bit_exact(bits, group):
+    N, K = 64, 512
+    w = _w(N, K, 200, bits, group)
+    p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+    wf = torch.empty((N, K), dtype=torch.float32, device=DEV)
+    wb = torch.empty((N, K), dtype=torch.int16, device=DEV)
+    ss.subspec_qdequant(p["qweight"], p["scales"], p["zeros"], bits, group, N, K, wf, wb)
+    torch.cuda.synchronize()
+    q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+    exp_f = oracle.dequant_f32(q, s16, z16, group)
+    exp_b = oracle.dequant_bf16_bits(q, s16, z16, group)
+    assert np.array_equal(wf.cpu().numpy().view(np.uint32), exp_f.view(np.uint32))
+    assert np.array_equal(wb.cpu().numpy().view(np.uint16), exp_b)
+
+
+# ------------------------------------------------------------------ the layer
+
+SHAPES = [(512, 256), (528, 640), (1040, 1152)]  # tiles x blocks incl. ragged groups/chunks
+
+
+@pytest.mark.parametrize("bits,group", [(4, 64), (4, 128), (3, 128), (3, 64), (2, 64), (2, 128)])
+@pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA])
+def test_qlinear_matches_oracle(bits, group, path):
+    ms = [1, 2, 3, 4, 5, 8] if path == ss.SUBSPEC_PATH_GEMV else [1, 8, 16, 17, 33, 64, 100, 128]
+    for (N, K) in SHAPES:
+        w = _w(N, K, 300, N, K, bits, group)
+        p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+        q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+        for M in ms:
+            x = synth.activations(M, K, 301, M, N, K)
+            y = run_qlinear(p, x.to(DEV), path)
+            y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, group)
+            assert_close(bf16_to_f64(y), y_ref, f"bits={bits} g={group} path={path} M={M} N={N} K={K}")
+
+
+@pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA])
+def test_qlinear_exact_integer_case(path):
+    # s=1, z=0, codes in {0,1}, x in {-1,0,1}: every partial sum is a small integer,
+    # so the GPU result must equal the oracle bit for bit.
+    M, N, K = (4 if path == ss.SUBSPEC_PATH_GEMV else 32), 64, 256
+    rng = np.random.default_rng(5)
+    codes = rng.integers(0, 2, (N, K)).astype(np.uint8)
+    xi = rng.integers(-1, 2, (M, K)).astype(np.float32)
+    qw = torch.empty(ss.subspec_qpack_bytes(4, N, K), dtype=torch.uint8, device=DEV)
+    ss.subspec_qpack(torch.from_numpy(codes).to(DEV), 4, N, K, qw)
+    sc = torch.ones((K // 128, N), dtype=torch.float16, device=DEV)
+    zr = torch.zeros((K // 128, N), dtype=torch.float16, device=DEV)
+    x = torch.from_numpy(xi).to(torch.bfloat16)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+    ss.subspec_qlinear_path(x.to(DEV), qw, sc, zr, 4, 128, M, N, K, y, path)
+    y_ref = oracle.qlinear_ref(synth.bf16_bits(x), codes, sc.cpu().numpy(), zr.cpu().numpy(), 128)
+    assert np.array_equal(bf16_to_f64(y), y_ref)
+
+
+def test_qlinear_deterministic():
+    N, K = 1040, 1152
+    w = _w(N, K, 400)
+    p = device_projection(torch.from_numpy(w).to(DEV), 3, 128)
+    for path, M in [(ss.SUBSPEC_PATH_GEMV, 5), (ss.SUBSPEC_PATH_MFMA, 40)]:
+        x = synth.activations(M, K, 401, M).to(DEV)
+        y1 = run_qlinear(p, x, path)
+        y2 = run_qlinear(p, x, path)
+        assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+def test_qlinear_outlier_activations():
+    # 1% of the input channels scaled by 20 (the aggressive 2-bit workload's inputs)
+    N, K = 512, 1280
+    w = _w(N, K, 500)
+    p = device_projection(torch.from_numpy(w).to(DEV), 2, 64)
+    q, s16, z16 = oracle.quantize_minmax(w, 2, 64)
+    for M in (4, 128):
+        x = synth.activations(M, K, 501, outlier_frac=0.01)
+        y = run_qlinear(p, x.to(DEV))
+        y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, 64)
+        assert_close(bf16_to_f64(y), y_ref, f"outliers M={M}")
+
+
+def test_qlinear_does_not_touch_outside_y():
+    N, K, M = 512, 256, 3
+    w = _w(N, K, 600)
+    p = device_projection(torch.from_numpy(w).to(DEV), 4, 64)
+    x = synth.activations(M, K, 601).to(DEV)
+    guard = torch.full((M * N + 2 * 4096,), -7, dtype=torch.int16, device=DEV)
+    y = guard[4096:4096 + M * N].view(torch.bfloat16).view(M, N)
+    for path in (ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA):
+        ss.subspec_qlinear_path(x, p["qweight"], p["scales"], p["zeros"], 4, 64, M, N, K, y, path)
+        torch.cuda.synchronize()
+        assert torch.all(guard[:4096] == -7) and torch.all(guard[4096 + M * N:] == -7)

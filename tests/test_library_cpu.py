@@ -1,0 +1,130 @@
+"""CPU-only checks of the native library: it loads, exports every entry point the
+header declares, validates arguments, plans launches, and its host packer writes
+the specified layout (pinned against hand-derived bytes and the oracle's reader)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2509_18344_amd as ss
+from paper_2509_18344_amd import _binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ss.load_library()
+    header = open(os.path.join(ROOT, "include", "subspec.h")).read()
+    names = set(re.findall(r"\b(subspec_[a-z_0-9]+)\s*\(", header))
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_qpack_bytes():
+    assert ss.subspec_qpack_bytes(4, 512, 256) == 512 * 256 // 2
+    assert ss.subspec_qpack_bytes(3, 16, 128) == 768
+    assert ss.subspec_qpack_bytes(2, 32, 256) == 2048
+    assert ss.subspec_qpack_bytes(5, 16, 128) == 0
+    assert ss.subspec_qpack_bytes(4, 8, 128) == 0
+    assert ss.subspec_qpack_bytes(4, 16, 100) == 0
+
+
+def _golden_rows(golden_dir):
+    rows = []
+    with open(os.path.join(golden_dir, "unpack_bytes.txt")) as f:
+        for ln in f:
+            if ln.strip() and not ln.startswith("#"):
+                rows.append(ln.split())
+    return rows
+
+
+def test_host_packer_matches_golden_bytes(golden_dir):
+    rows = _golden_rows(golden_dir)
+    for bits in (2, 3, 4):
+        codes = np.zeros((16, 128), np.uint8)
+        expect = np.zeros(256 * bits, np.uint8)
+        for b, n, k, q, off, val in rows:
+            if int(b) != bits:
+                continue
+            codes[int(n), int(k)] = int(q)
+            expect[int(off)] |= int(val, 16)
+        out = np.zeros(256 * bits, np.uint8)
+        ss.subspec_qpack_host(codes, bits, 16, 128, out)
+        assert np.array_equal(out, expect), bits
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_host_packer_round_trip_exhaustive(bits):
+    # every code value at every position of a tile, plus a random multi-tile matrix
+    N, K = 16, 128
+    for v in range(2 ** bits):
+        codes = np.full((N, K), v, np.uint8)
+        out = np.zeros(N * K * bits // 8, np.uint8)
+        ss.subspec_qpack_host(codes, bits, N, K, out)
+        assert np.array_equal(oracle.unpack(out, bits, N, K), codes)
+    rng = np.random.default_rng(bits)
+    for N, K in [(16, 128), (48, 384), (32, 1024)]:
+        codes = rng.integers(0, 2 ** bits, (N, K)).astype(np.uint8)
+        out = np.zeros(N * K * bits // 8, np.uint8)
+        ss.subspec_qpack_host(codes, bits, N, K, out)
+        assert np.array_equal(oracle.unpack(out, bits, N, K), codes)
+
+
+@pytest.mark.parametrize("M,N,K,bits,group,path,err", [
+    (1, 512, 256, 5, 64, 0, "EUNSUPPORTED"),
+    (1, 512, 256, 4, 32, 0, "EUNSUPPORTED"),
+    (1, 512, 200, 4, 64, 0, "EUNSUPPORTED"),
+    (1, 520, 256, 4, 64, 0, "EUNSUPPORTED"),
+    (0, 512, 256, 4, 64, 0, "EUNSUPPORTED"),
+    (129, 512, 256, 4, 64, 0, "EUNSUPPORTED"),
+    (9, 512, 256, 4, 64, 1, "EUNSUPPORTED"),
+    (4, 512, 256, 4, 64, 7, "EINVAL"),
+    (4, -16, 256, 4, 64, 0, "EINVAL"),
+])
+def test_plan_rejects_bad_shapes(M, N, K, bits, group, path, err):
+    with pytest.raises(ss.SubspecError) as ei:
+        ss.subspec_qlinear_plan(M, N, K, bits, group, path)
+    assert err in str(ei.value)
+
+
+def test_plan_choices_are_consistent():
+    for M in (1, 2, 3, 4, 5, 8, 9, 16, 17, 32, 33, 64, 65, 100, 128):
+        for (N, K) in [(512, 256), (18944, 3584), (3584, 18944), (55296, 5120), (5120, 27648)]:
+            for bits, group in [(4, 128), (3, 128), (2, 64), (4, 64)]:
+                p = ss.subspec_qlinear_plan(M, N, K, bits, group)
+                assert p["rows"] >= M
+                KB = K // 128
+                assert p["splits"] >= 1 and p["blocks_per_split"] % p["chunk_blocks"] == 0
+                assert (p["splits"] - 1) * p["blocks_per_split"] < KB <= p["splits"] * p["blocks_per_split"]
+                cols = 4 * p["tiles_per_wave"] * 16
+                assert p["col_groups"] == -(-N // cols)
+                assert p["grid"] == p["col_groups"] * p["splits"]
+                if p["splits"] == 1:
+                    assert p["workspace_bytes"] == 0
+                else:
+                    assert p["workspace_bytes"] >= p["splits"] * M * N * 4 + 4 * p["col_groups"]
+    assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_GEMV
+    assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_MFMA)["path"] == ss.SUBSPEC_PATH_MFMA
+
+
+def test_qlinear_argument_errors_need_no_gpu():
+    with pytest.raises(ss.SubspecError) as ei:
+        ss.subspec_qlinear(None, 16, 16, 16, 4, 64, 1, 512, 256, 16, stream=0)
+    assert "EINVAL" in str(ei.value) and "null" in ss.subspec_last_error()
+    with pytest.raises(ss.SubspecError) as ei:
+        ss.subspec_qlinear(16, 16, 16, 24, 4, 64, 1, 512, 256, 16, stream=0)
+    assert "aligned" in ss.subspec_last_error()
+    with pytest.raises(ss.SubspecError):
+        ss.subspec_qlinear_path(16, 16, 16, 16, 4, 64, 9, 512, 256, 16, ss.SUBSPEC_PATH_GEMV, stream=0)
+    with pytest.raises(ss.SubspecError):
+        ss.subspec_quantize(16, 4, 64, 16, 100, 16, 16, 16, stream=0)
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_binding, "_lib", None)
+    monkeypatch.setattr(_binding, "_HERE", str(tmp_path))
+    with pytest.raises(RuntimeError, match="missing"):
+        _binding.load_library()
