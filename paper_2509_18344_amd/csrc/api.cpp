@@ -124,6 +124,12 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   const int chunks = (KB + c.chunk - 1) / c.chunk;
   int splits = (tu.target_blocks + col_groups - 1) / col_groups;
   if (splits < 1) splits = 1;
+  if (c.path == 1) {
+    // the split's activations must fit the GEMV kernel's LDS staging
+    const int max_chunks = subspec::gemv_max_kspan(c.rows) / subspec::kTileK / c.chunk;
+    const int min_splits = (chunks + max_chunks - 1) / max_chunks;
+    if (splits < min_splits) splits = min_splits;
+  }
   if (splits > chunks) splits = chunks;
   int chunks_per_split = (chunks + splits - 1) / splits;
   const int blocks_per_split = chunks_per_split * c.chunk;
@@ -137,10 +143,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   p->blocks_per_split = blocks_per_split;
   p->grid = col_groups * splits;
   p->workspace_bytes = 0;
-  if (splits > 1) {
-    const size_t counters = (static_cast<size_t>(col_groups) * 4 + 255) / 256 * 256;
-    p->workspace_bytes = counters + static_cast<size_t>(splits) * M * N * sizeof(float);
-  }
+  if (splits > 1) p->workspace_bytes = static_cast<size_t>(splits) * M * N * sizeof(float);
   if (kc) *kc = c;
   return SUBSPEC_OK;
 }
@@ -161,7 +164,7 @@ int current_device(int* dev) {
 }
 
 // Returns the device's workspace, grown to `bytes` if needed.  Growth allocates
-// (synchronously) and zero-fills, so it is refused while `st` is being captured.
+// synchronously, so it is refused while `st` is being captured.
 int get_workspace(size_t bytes, hipStream_t st, void** out) {
   int dev = 0;
   int rc = current_device(&dev);
@@ -194,11 +197,6 @@ int get_workspace(size_t bytes, hipStream_t st, void** out) {
   void* p = nullptr;
   e = hipMalloc(&p, nb);
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
-  e = hipMemset(p, 0, nb);
-  if (e != hipSuccess) {
-    hipFree(p);
-    return hip_fail(e, "hipMemset(workspace)");
-  }
   w.ptr = p;
   w.bytes = nb;
   *out = p;
@@ -269,9 +267,7 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
     void* ws = nullptr;
     rc = get_workspace(p.workspace_bytes, st, &ws);
     if (rc) return rc;
-    const size_t counters = (static_cast<size_t>(p.col_groups) * 4 + 255) / 256 * 256;
-    a.counters = static_cast<unsigned*>(ws);
-    a.ws = reinterpret_cast<float*>(static_cast<char*>(ws) + counters);
+    a.ws = static_cast<float*>(ws);
   }
   hipError_t e = subspec::launch_qlinear(kc, bits, group, a, p.grid, st);
   if (e != hipSuccess) return hip_fail(e, "qlinear launch");

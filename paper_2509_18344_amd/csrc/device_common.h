@@ -41,36 +41,46 @@ __device__ __forceinline__ Slice<BITS> load_slice(const uint8_t* __restrict__ p)
   return s;
 }
 
+// (a & mask) | bias in one VALU instruction: gfx950's three-input bitwise
+// v_bitop3_b32 with truth table 0xEA (inputs weighted 0xF0, 0xCC, 0xAA).  Through
+// the builtin, not inline assembly, so the compiler sees the instruction and keeps
+// the wait states a matrix-core read of its result needs.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t mask, uint32_t bias) {
+  return __builtin_amdgcn_bitop3_b32(a, mask, bias, 0xEA);
+}
+
 // Unpack a slice into its 16 pairs.  pr[p] holds (0x4300 | q_even) in the low and
 // (0x4300 | q_odd) in the high 16 bits, i.e. two bf16 values 128 + q; pair p covers
 // elements e = 2*(p%4), 2*(p%4)+1 of step p/4.
 template <int BITS>
 __device__ __forceinline__ void unpack_pairs(const Slice<BITS>& s, uint32_t pr[16]) {
+  const uint32_t bias = kPairBias;
   if constexpr (BITS == 4) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t d = s.w[j];
-      pr[4 * j + 0] = (d & 0x000F000Fu) | kPairBias;
-      pr[4 * j + 1] = ((d >> 4) & 0x000F000Fu) | kPairBias;
-      pr[4 * j + 2] = ((d >> 8) & 0x000F000Fu) | kPairBias;
-      pr[4 * j + 3] = ((d >> 12) & 0x000F000Fu) | kPairBias;
+      pr[4 * j + 0] = and_or(d, 0x000F000Fu, bias);
+      pr[4 * j + 1] = and_or(d >> 4, 0x000F000Fu, bias);
+      pr[4 * j + 2] = and_or(d >> 8, 0x000F000Fu, bias);
+      pr[4 * j + 3] = and_or(d >> 12, 0x000F000Fu, bias);
     }
   } else if constexpr (BITS == 2) {
 #pragma unroll
     for (int w = 0; w < 2; ++w) {
       const uint32_t d = s.w[w];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) pr[8 * w + t] = ((d >> (2 * t)) & 0x00030003u) | kPairBias;
+      for (int t = 0; t < 8; ++t) pr[8 * w + t] = and_or(d >> (2 * t), 0x00030003u, bias);
     }
   } else {
 #pragma unroll
     for (int w = 0; w < 3; ++w) {
       const uint32_t d = s.w[w];
 #pragma unroll
-      for (int t = 0; t < 5; ++t) pr[5 * w + t] = ((d >> (3 * t)) & 0x00070007u) | kPairBias;
+      for (int t = 0; t < 5; ++t) pr[5 * w + t] = and_or(d >> (3 * t), 0x00070007u, bias);
     }
-    pr[15] = ((s.w[0] >> 15) & 0x00010001u) | ((s.w[1] >> 14) & 0x00020002u) |
-             ((s.w[2] >> 13) & 0x00040004u) | kPairBias;
+    uint32_t p15 = and_or(s.w[0] >> 15, 0x00010001u, bias);
+    p15 = and_or(s.w[1] >> 14, 0x00020002u, p15);
+    pr[15] = and_or(s.w[2] >> 13, 0x00040004u, p15);
   }
 }
 

@@ -20,7 +20,6 @@ struct QArgs {
   const uint16_t* zr;     // fp16 [K/group][N]
   uint16_t* y;            // bf16 [M][N]
   float* ws;              // fp32 [splits][M][N] partial sums (splits > 1)
-  unsigned* counters;     // [col_groups] arrival counters, zero between calls
   int M, N, K;
   int KB;                 // K / 128
   int n_tiles;            // N / 16
@@ -38,6 +37,10 @@ struct KernelChoice {
 hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a,
                           int grid, hipStream_t st);
 bool qlinear_variant_exists(const KernelChoice& kc, int bits, int group);
+// GEMV path: the whole split's activations live in LDS, so a split may span at most
+// gemv_max_kspan(rows) inputs; gemv_lds_bytes is the dynamic LDS of one workgroup.
+int gemv_max_kspan(int rows);
+size_t gemv_lds_bytes(int rows, int kspan, int group);
 
 hipError_t launch_quantize(const float* w, int bits, int group, int N, int K, uint8_t* codes,
                            uint16_t* sc, uint16_t* zr, hipStream_t st);
