@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--cpu-sample-cols", type=int, default=1 << 30)
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 GEMV, 2 MFMA")
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (reference "
+                         "for the HBM traffic counters) and exit")
     return ap.parse_args()
 
 
@@ -130,6 +133,15 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration_mb:
+        n = args.copy_calibration_mb << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n}))
+        return
     ss.load_library()
     wl = WORKLOADS[args.workload]
     ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else wl.ms

@@ -80,12 +80,13 @@ typedef struct subspec_plan {
   int path;            /* SUBSPEC_PATH_GEMV or SUBSPEC_PATH_MFMA                  */
   int rows;            /* rows computed per workgroup (M rounded up)              */
   int tiles_per_wave;  /* 16-column tiles each wavefront owns                     */
+  int waves;           /* wavefronts per workgroup                                */
   int chunk_blocks;    /* 128-k blocks staged in LDS per step                     */
   int col_groups;      /* workgroups along N                                      */
   int splits;          /* workgroups along K (split-K); 1 = no partial results    */
   int blocks_per_split;/* 128-k blocks per split                                  */
   int grid;            /* total workgroups = col_groups * splits                  */
-  size_t workspace_bytes; /* device scratch needed (fp32 partials + counters)    */
+  size_t workspace_bytes; /* device scratch needed: fp32 partial sums of the splits */
 } subspec_plan;
 
 /* Bytes of the packed code buffer for an N x K projection.  0 on bad arguments. */

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -57,9 +58,11 @@ constexpr int kGemvMaxRows = 8;
 
 struct Tuning {
   int gemv_max_m = kGemvMaxRows;  // largest M the automatic plan sends to the GEMV path
-  int target_blocks = 1024;       // workgroups the split-K choice aims for
+  int target_blocks = 0;          // workgroups to aim for; 0 = one full residency round
   int gemv_nt = 1;
-  int mfma_nt = 2;
+  int mfma_nt = 0;                // 0 = choose per shape
+  int splits = 0;                 // 0 = choose per shape
+  int partial_div = 2;            // split-K partial traffic may reach weight bytes / this
 };
 
 // Optional overrides for measurement sweeps: SUBSPEC_TUNE="gemv_max_m=4,target=512,...".
@@ -82,12 +85,29 @@ const Tuning& tuning() {
         else if (k == "target") r.target_blocks = v;
         else if (k == "gemv_nt") r.gemv_nt = v;
         else if (k == "mfma_nt") r.mfma_nt = v;
+        else if (k == "splits") r.splits = v;
+        else if (k == "partial_div") r.partial_div = v;
       }
       pos = end + 1;
     }
     return r;
   }();
   return t;
+}
+
+// Compute units of the current device (256 on MI355X; the fallback when no GPU is
+// present keeps host-only planning deterministic).
+int device_cus() {
+  static int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      return 256;
+    }
+    return n;
+  }();
+  return cus;
 }
 
 int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* p,
@@ -99,7 +119,10 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   if (M < 1 || M > kMaxRows) return fail(SUBSPEC_EUNSUPPORTED, "M=%d: must be in 1..%d", M, kMaxRows);
   const Tuning& tu = tuning();
   if (path == SUBSPEC_PATH_AUTO) path = (M <= tu.gemv_max_m) ? SUBSPEC_PATH_GEMV : SUBSPEC_PATH_MFMA;
+  const int KB = K / subspec::kTileK;
+  const int n_tiles = N / subspec::kTileN;
   subspec::KernelChoice c{};
+  c.waves = 4;
   if (path == SUBSPEC_PATH_GEMV) {
     if (M > kGemvMaxRows) return fail(SUBSPEC_EUNSUPPORTED, "GEMV path needs M <= 8 (M=%d)", M);
     c.path = 1;
@@ -110,23 +133,43 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c.path = 2;
     const int mt = M <= 16 ? 1 : M <= 32 ? 2 : M <= 64 ? 4 : 8;
     c.rows = 16 * mt;
-    c.nt = tu.mfma_nt;
-    c.chunk = mt == 1 ? 4 : mt == 8 ? 1 : 2;
+    // LDS holds two chunks of rows x (128*chunk) activations: ~34 KB up to M = 64.
+    c.chunk = mt == 1 ? 4 : mt == 2 ? 2 : 1;
+    // Two tiles per wavefront halve the activation reads from LDS; one tile per
+    // wavefront doubles the workgroups for narrow projections.
+    c.nt = tu.mfma_nt ? tu.mfma_nt : ((n_tiles / 8) >= device_cus() ? 2 : 1);
   } else {
     return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
   }
   if (!subspec::qlinear_variant_exists(c, bits, group))
-    return fail(SUBSPEC_EUNSUPPORTED, "no kernel for path=%d rows=%d nt=%d chunk=%d bits=%d group=%d",
-                c.path, c.rows, c.nt, c.chunk, bits, group);
-  const int KB = K / subspec::kTileK;
-  const int cols_per_group = subspec::kWavesPerBlock * c.nt * subspec::kTileN;
+    return fail(SUBSPEC_EUNSUPPORTED, "no kernel for path=%d rows=%d nt=%d chunk=%d waves=%d bits=%d group=%d",
+                c.path, c.rows, c.nt, c.chunk, c.waves, bits, group);
+  const int cols_per_group = c.waves * c.nt * subspec::kTileN;
   const int col_groups = (N + cols_per_group - 1) / cols_per_group;
   const int chunks = (KB + c.chunk - 1) / c.chunk;
-  int splits = (tu.target_blocks + col_groups - 1) / col_groups;
-  if (splits < 1) splits = 1;
+
+  // Split K across workgroups only as far as one residency round reaches, and only
+  // while the fp32 partial sums (written once, read once) stay a modest fraction of
+  // the weight bytes.
+  int resident = 0;
+  if (tu.target_blocks > 0) {
+    resident = tu.target_blocks;
+  } else {
+    size_t lds = 0;
+    if (c.path == 1) lds = subspec::gemv_lds_bytes(c.rows, std::min(K, subspec::gemv_max_kspan(c.rows, c.waves)), group);
+    int per_cu = subspec::qlinear_resident_blocks(c, bits, group, lds);
+    if (per_cu <= 0) per_cu = 2;
+    resident = per_cu * device_cus();
+  }
+  int splits = std::max(1, resident / col_groups);
+  const double wbytes = static_cast<double>(N) * K * bits / 8 + 4.0 * N * (K / group);
+  const double per_split = 8.0 * M * N;
+  const int cap = std::max(1, static_cast<int>(wbytes / (tu.partial_div * per_split)));
+  splits = std::min(splits, cap);
+  if (tu.splits > 0) splits = tu.splits;
   if (c.path == 1) {
     // the split's activations must fit the GEMV kernel's LDS staging
-    const int max_chunks = subspec::gemv_max_kspan(c.rows) / subspec::kTileK / c.chunk;
+    const int max_chunks = subspec::gemv_max_kspan(c.rows, c.waves) / subspec::kTileK / c.chunk;
     const int min_splits = (chunks + max_chunks - 1) / max_chunks;
     if (splits < min_splits) splits = min_splits;
   }
@@ -137,6 +180,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   p->path = path;
   p->rows = c.rows;
   p->tiles_per_wave = c.nt;
+  p->waves = c.waves;
   p->chunk_blocks = c.chunk;
   p->col_groups = col_groups;
   p->splits = splits;

@@ -12,6 +12,9 @@ namespace subspec {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+// Native 128-bit vector (HIP's uint4 is a wrapper struct that register promotion
+// does not always split).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // Bias added to every unpacked code: the 16-bit field 0x4300 | q is the bf16 value
 // 128 + q exactly (exponent 2^7, seven mantissa bits of weight 1), for q < 128.

@@ -32,14 +32,17 @@ struct KernelChoice {
   int rows;    // GEMV: 1, 2, 4, 8; MFMA: 16 * m-tiles
   int nt;      // tiles per wavefront
   int chunk;   // 128-k blocks per LDS stage
+  int waves;   // wavefronts per workgroup (4 or 8)
 };
 
 hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a,
                           int grid, hipStream_t st);
 bool qlinear_variant_exists(const KernelChoice& kc, int bits, int group);
+// Workgroups of this variant that fit on one compute unit (0 if unknown, e.g. no GPU).
+int qlinear_resident_blocks(const KernelChoice& kc, int bits, int group, size_t dyn_lds);
 // GEMV path: the whole split's activations live in LDS, so a split may span at most
 // gemv_max_kspan(rows) inputs; gemv_lds_bytes is the dynamic LDS of one workgroup.
-int gemv_max_kspan(int rows);
+int gemv_max_kspan(int rows, int waves);
 size_t gemv_lds_bytes(int rows, int kspan, int group);
 
 hipError_t launch_quantize(const float* w, int bits, int group, int N, int K, uint8_t* codes,
@@ -48,7 +51,6 @@ hipError_t launch_qpack(const uint8_t* codes, int bits, int N, int K, void* qw, 
 hipError_t launch_qdequant(const void* qw, const void* sc, const void* zr, int bits, int group,
                            int N, int K, float* wf, uint16_t* wb, hipStream_t st);
 
-constexpr int kWavesPerBlock = 4;
-constexpr int kThreadsPerBlock = 256;
+constexpr int kThreadsPerBlock = 256;  // split-K reduction kernel
 
 }  // namespace subspec

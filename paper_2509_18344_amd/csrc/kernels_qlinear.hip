@@ -1,12 +1,14 @@
 // The substitute-layer linear y = x * dequant(q, s, z)^T (SubSpec Sec. 4.1) for
 // draft-tree batches, as two kernels over one packed layout:
 //
-//   k_qgemv       M <= 8.  VALU bf16 dot products; the four 16-lane quarters of a
-//                 wavefront split K inside every tile and are reduced with cross-row
-//                 lane swaps at the end, workgroups split K through a fixed-order
-//                 reduction of fp32 partial sums.
+//   k_qgemv       small M.  VALU bf16 dot products; the four 16-lane quarters of a
+//                 wavefront split K inside every tile and are summed with cross-row
+//                 lane exchanges at the end.
 //   k_qgemm_mfma  any M.  16x16x32 bf16 MFMA; the A operand (activations) comes
 //                 from LDS, the B operand straight from the unpacked codes.
+//
+// Both split K across workgroups when a projection has too few columns to fill the
+// GPU; the fp32 partial sums are then added in split order by k_splitk_reduce.
 //
 // Dequantization is folded into the accumulation.  Within one group the weight is
 // affine in the code, W^ = s*(q - z), so for every (row m, column n, group g)
@@ -15,112 +17,101 @@
 // device_common.h) to the dot products / matrix cores and apply s and z once per
 // (m, n, g).  The effective weights are the exact dequantized values; the only
 // roundings are the fp32 accumulation and the final bf16 store.
+#include <type_traits>
+#include <utility>
+
 #include "device_common.h"
 #include "kernels.h"
 
 namespace subspec {
 
 // ---------------------------------------------------------------------------
-// Activation staging: one chunk (CHUNK blocks of 128 k, all ROWS rows) of x is
-// copied to LDS by the whole workgroup together with the per-group sums of x the
-// zero-point correction needs.  Double buffered: chunk c+1 is read from global
-// memory into registers while chunk c is being consumed.
+// Small helpers.
 // ---------------------------------------------------------------------------
 
-template <int ROWS, int CHUNK, int GROUP, bool QUARTER>
-struct StageLds {
-  static constexpr int CK = CHUNK * kTileK;
-  static constexpr int XSTRIDE = CK + 8;  // bf16 per row, +16 bytes against bank conflicts
-  static constexpr int GPC = CK / GROUP;  // groups per chunk
-  static constexpr int SUMS = QUARTER ? 4 : 1;
-  uint16_t x[2][ROWS][XSTRIDE];
-  // Sum of x over one group (MFMA) or over the quarter of a group one 16-lane
-  // quarter of a wavefront sees (GEMV: k % 32 in [8q, 8q+8)).
-  float xsum[2][GPC][ROWS][SUMS];
-};
-
-template <int ROWS, int CHUNK>
-struct StageRegs {
-  static constexpr int C8 = CHUNK * 16;  // 16-byte pieces per row of a chunk
-  static constexpr int TOTAL = ROWS * C8;
-  static constexpr int NPASS = (TOTAL + kThreadsPerBlock - 1) / kThreadsPerBlock;
-  uint4 v[NPASS];
-};
-
-// Loads are unconditional: out-of-range pieces read a clamped (valid) address and
-// are never consumed (blocks past the split are skipped, rows past M never stored),
-// so no branch -- and no early wait on the counter of outstanding loads -- is
-// placed around them.
-template <int ROWS, int CHUNK>
-__device__ __forceinline__ void stage_load(StageRegs<ROWS, CHUNK>& r, const QArgs& a, int kb,
-                                           int kb_end) {
-  using R = StageRegs<ROWS, CHUNK>;
-#pragma unroll
-  for (int p = 0; p < R::NPASS; ++p) {
-    const int i = p * kThreadsPerBlock + threadIdx.x;
-    const int row = min(i / R::C8, a.M - 1), c8 = i % R::C8;
-    const int kbc = min(kb + c8 / 16, kb_end - 1);
-    r.v[p] = *reinterpret_cast<const uint4*>(a.x + static_cast<size_t>(row) * a.K +
-                                             static_cast<size_t>(kbc) * kTileK + (c8 % 16) * 8);
-  }
+// Calls f(std::integral_constant<int, 0>{}) ... f(integral_constant<int, N-1>{}): ring
+// slots indexed by a compile-time constant stay in registers.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-__device__ __forceinline__ float bf16lo(uint32_t v) { return __builtin_bit_cast(float, v << 16); }
-__device__ __forceinline__ float bf16hi(uint32_t v) { return __builtin_bit_cast(float, v & 0xFFFF0000u); }
+__device__ __forceinline__ float dot2_bf16(uint32_t xa, uint32_t wb, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xa),
+                                         __builtin_bit_cast(bf16x2_t, wb), acc, false);
+}
 
-// DPP move of a float within 16-lane rows (all lanes active).
+// Sum of the eight bf16 values of a 16-byte piece (dot products with 1.0 pairs).
+__device__ __forceinline__ float piece_sum(const u32x4_t& v, float acc) {
+  constexpr uint32_t kOnes = 0x3F803F80u;  // bf16 1.0, 1.0
+  acc = dot2_bf16(v.x, kOnes, acc);
+  acc = dot2_bf16(v.y, kOnes, acc);
+  acc = dot2_bf16(v.z, kOnes, acc);
+  return dot2_bf16(v.w, kOnes, acc);
+}
+
+// DPP move of a float within rows of 16 lanes (all lanes active).
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
                                                                0xF, 0xF, false));
 }
-constexpr int kDppQuadXor1 = 0xB1;      // quad_perm [1,0,3,2]
-constexpr int kDppQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]
-constexpr int kDppRowRor4 = 0x124;      // row_ror:4
-constexpr int kDppRowRor8 = 0x128;      // row_ror:8
-constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
 
-template <int ROWS, int CHUNK, int GROUP, bool QUARTER>
-__device__ __forceinline__ void stage_store(StageLds<ROWS, CHUNK, GROUP, QUARTER>& L, int buf,
-                                            const StageRegs<ROWS, CHUNK>& r) {
-  using R = StageRegs<ROWS, CHUNK>;
-  constexpr int P8 = GROUP / 8;  // 16-byte pieces per group
+// Sum over the lanes of an aligned group of SPAN lanes (SPAN = 1, 2 or 4).
+template <int SPAN>
+__device__ __forceinline__ float span_reduce(float v) {
+  if constexpr (SPAN >= 2) v += dpp_f<kDppQuadXor1>(v);
+  if constexpr (SPAN >= 4) v += dpp_f<kDppQuadXor2>(v);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Activation staging.  The unit of work is a "span": 32 consecutive k of one row
+// (four 16-byte pieces) read by one thread, so that the thread can sum its own
+// values; the spans of one group of k are G/32 consecutive threads (2 or 4 lanes of
+// one DPP quad) and are reduced with one or two quad permutes.  Piece p of a span
+// holds the k with k % 32 in [8p, 8p+8): the slice of a group one 16-lane quarter
+// of a wavefront multiplies (quarter p).
+//
+// Loads are unconditional: out-of-range spans read a clamped (valid) address and
+// are never consumed (blocks past the split are skipped, rows past M never stored),
+// so no branch -- and no early wait on outstanding loads -- surrounds them.
+// ---------------------------------------------------------------------------
+
+template <int SPANS_PER_THREAD>
+struct SpanRegs {
+  u32x4_t v[SPANS_PER_THREAD][4];
+};
+
+// Load spans i = p*THREADS + tid (p < SPT) of a rows x (nblk blocks) region starting
+// at block kb; a row holds nblk*4 spans.
+template <int SPT, int THREADS>
+__device__ __forceinline__ void load_spans(SpanRegs<SPT>& r, const QArgs& a, int kb, int kb_end,
+                                           int spans_per_row, int total) {
 #pragma unroll
-  for (int p = 0; p < R::NPASS; ++p) {
-    const int i = p * kThreadsPerBlock + threadIdx.x;
-    const int row = i / R::C8, c8 = i % R::C8;
-    const uint4 v = r.v[p];
-    if (i < R::TOTAL) *reinterpret_cast<uint4*>(&L.x[buf][row][c8 * 8]) = v;
-    float s = ((bf16lo(v.x) + bf16hi(v.x)) + (bf16lo(v.y) + bf16hi(v.y))) +
-              ((bf16lo(v.z) + bf16hi(v.z)) + (bf16lo(v.w) + bf16hi(v.w)));
-    // The pieces of one (row, group) are P8 consecutive lanes of one 16-lane row.
-    if constexpr (QUARTER) {
-      // quarter q of a group = pieces with c8 % 4 == q
-      if constexpr (GROUP == 128) {
-        s += dpp_f<kDppRowRor4>(s);
-        s += dpp_f<kDppRowRor8>(s);
-      } else {
-        s += __shfl_xor(s, 4);
-      }
-      if (i < R::TOTAL && (c8 % P8) < 4) L.xsum[buf][c8 / P8][row][c8 % 4] = s;
-    } else {
-      s += dpp_f<kDppQuadXor1>(s);
-      s += dpp_f<kDppQuadXor2>(s);
-      if constexpr (GROUP == 128) {
-        s += dpp_f<kDppRowRor4>(s);
-        s += dpp_f<kDppRowRor8>(s);
-      } else {
-        s += dpp_f<kDppRowHalfMirror>(s);
-      }
-      if (i < R::TOTAL && (c8 % P8) == 0) L.xsum[buf][c8 / P8][row][0] = s;
-    }
+  for (int p = 0; p < SPT; ++p) {
+    const int i = min(p * THREADS + static_cast<int>(threadIdx.x), total - 1);
+    const int row = min(i / spans_per_row, a.M - 1);
+    const int sp = i % spans_per_row;
+    const int kbc = min(kb + sp / 4, kb_end - 1);
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(a.x + static_cast<size_t>(row) * a.K +
+                                                          static_cast<size_t>(kbc) * kTileK +
+                                                          (sp % 4) * 32);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r.v[p][q] = src[q];
   }
 }
 
 // ---------------------------------------------------------------------------
 // Weight stream: every wavefront owns NT tiles (16 columns each) and walks its
-// split's k-blocks in chunks of CH blocks.  Two chunks of slices and their raw
-// fp16 scale/zero values are in flight at any time (ping-pong registers).
+// split's k-blocks in chunks of CH blocks; a ring of PF chunks (slices and raw fp16
+// scale/zero values) is in flight at any time.
 // ---------------------------------------------------------------------------
 
 template <int BITS, int NT, int CH, int GPC>
@@ -130,8 +121,8 @@ struct WChunk {
   uint32_t z[GPC][NT];  // fp16 bits of the zero-point
 };
 
-// Unconditional loads from clamped addresses (see stage_load): blocks past the end
-// of the split re-read its last block and are never consumed.
+// Unconditional loads from clamped addresses: blocks past the end of the split
+// re-read its last block and are never consumed.
 template <int BITS, int GROUP, int NT, int CH, int GPC>
 __device__ __forceinline__ void load_wchunk(WChunk<BITS, NT, CH, GPC>& r, const QArgs& a,
                                             const uint8_t* const (&wbase)[NT],
@@ -184,11 +175,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void k_splitk_reduce(const float*
   const size_t quads = static_cast<size_t>(M) * N / 4;
   const size_t i = static_cast<size_t>(blockIdx.x) * kThreadsPerBlock + threadIdx.x;
   if (i >= quads) return;
-  const size_t plane = static_cast<size_t>(M) * N / 4;
   const float4* src = reinterpret_cast<const float4*>(ws) + i;
   float4 acc = src[0];
   for (int sp = 1; sp < splits; ++sp) {
-    const float4 v = src[sp * plane];
+    const float4 v = src[sp * quads];
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
   const uint32_t lo = static_cast<uint32_t>(float_to_bf16_bits(acc.x)) |
@@ -198,26 +188,95 @@ __global__ __launch_bounds__(kThreadsPerBlock) void k_splitk_reduce(const float*
   reinterpret_cast<uint2*>(y)[i] = make_uint2(lo, hi);
 }
 
+// Tile ownership shared by both kernels.
+template <int BITS, int NT>
+struct TileSet {
+  const uint8_t* wbase[NT];
+  bool ok[NT];
+  int ncol[NT];
+  __device__ __forceinline__ TileSet(const QArgs& a, int nt0, int lane) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      ok[t] = nt0 + t < a.n_tiles;
+      const int ntc = ok[t] ? nt0 + t : 0;
+      wbase[t] = a.qw + static_cast<size_t>(ntc) * a.KB * (256 * BITS) + lane * (4 * BITS);
+      ncol[t] = ntc * kTileN + (lane & 15);
+    }
+  }
+};
+
 // ---------------------------------------------------------------------------
-// MFMA kernel.  Workgroup = 4 wavefronts x NT tiles = 64*NT columns, all rows, one
-// k-split.  Per chunk of CH blocks: x is staged in LDS (double buffered, one
-// barrier per chunk); each wavefront unpacks its tiles' codes straight into B
-// operands and runs 16x16x32 bf16 MFMAs against A fragments read from LDS.
+// MFMA kernel.  Workgroup = WAVES wavefronts x NT tiles, all rows, one k-split.  Per
+// chunk of CH blocks, x is copied to LDS (double buffered, one barrier per chunk);
+// each wavefront unpacks its tiles' codes straight into B operands and runs
+// 16x16x32 bf16 MFMAs against A fragments read from LDS.  The per-group sums of x
+// that the zero-point needs come from one more MFMA per A fragment with an all-ones
+// B operand, which lands them in the accumulator layout with no extra VALU work.
+//
+// LDS layout of a chunk: 16-byte pieces, row-major [row][block][piece], the 16
+// pieces of each (row, block) permuted by piece ^ (row & 7).  Copy-in writes eight
+// consecutive pieces of one row per 8 lanes and an A fragment reads one piece of
+// eight consecutive rows per 8 lanes: both touch eight distinct 16-byte bank groups.
 // ---------------------------------------------------------------------------
 
-template <int BITS, int GROUP, int MT, int NT, int CH>
+template <int ROWS, int CH>
+struct MfmaLds {
+  static constexpr int PIECES = ROWS * CH * 16;
+  u32x4_t x[2][PIECES];
+};
+
+template <int BITS, int GROUP, int MT, int NT, int CH, int WAVES>
 struct MfmaBody {
   static constexpr int ROWS = 16 * MT;
+  static constexpr int THREADS = WAVES * kWave;
   static constexpr int GPB = kTileK / GROUP;  // groups per block
   static constexpr int SPG = 4 / GPB;         // 32-k steps per group
   static constexpr int GPC = CH * GPB;        // groups per chunk
-  using Lds = StageLds<ROWS, CH, GROUP, false>;
+  static constexpr int PIECES = ROWS * CH * 16;
+  static constexpr int PPT = PIECES / THREADS;  // pieces per thread per chunk
+  static_assert(PIECES % THREADS == 0, "a chunk is a whole number of pieces per thread");
+  using Lds = MfmaLds<ROWS, CH>;
   using W = WChunk<BITS, NT, CH, GPC>;
+  struct X {
+    u32x4_t v[PPT];
+  };
 
-  // Consume one chunk (blocks kb..kb+CH-1 of the split, LDS buffer buf).
+  static __device__ __forceinline__ int slot(int row, int b, int piece) {
+    return row * (CH * 16) + b * 16 + (piece ^ (row & 7));
+  }
+
+  // Coalesced copy of chunk (rows x blocks kb..kb+CH-1) into registers; rows past M
+  // and blocks past the split read clamped addresses and are never consumed.
+  static __device__ __forceinline__ void stage_load(X& r, const QArgs& a, int kb, int kb_end) {
+#pragma unroll
+    for (int p = 0; p < PPT; ++p) {
+      const int P = p * THREADS + threadIdx.x;
+      const int row = min(P / (CH * 16), a.M - 1), b = (P / 16) % CH, pc = P % 16;
+      const int kbc = min(kb + b, kb_end - 1);
+      r.v[p] = *reinterpret_cast<const u32x4_t*>(a.x + static_cast<size_t>(row) * a.K +
+                                                 static_cast<size_t>(kbc) * kTileK + pc * 8);
+    }
+  }
+
+  static __device__ __forceinline__ void stage_store(Lds& L, int buf, const X& r) {
+#pragma unroll
+    for (int p = 0; p < PPT; ++p) {
+      const int P = p * THREADS + threadIdx.x;
+      const int row = P / (CH * 16), b = (P / 16) % CH, pc = P % 16;
+      L.x[buf][slot(row, b, pc)] = r.v[p];
+    }
+  }
+
+  // Consume one chunk (blocks kb..kb+CH-1 of the split, LDS buffer buf).  Within a
+  // group the k-steps are outermost, so the MT*(NT+1) accumulators of the group form
+  // independent MFMA chains that keep the matrix pipe busy; each is folded into tot
+  // (scale and offset) when the group is complete.
   static __device__ __forceinline__ void compute(const W& wc, const Lds& lds, int buf, int kb,
-                                                 int kb_end, int col, int quarter,
-                                                 f32x4_t (&tot)[MT][NT]) {
+                                                 int kb_end, int lane, f32x4_t (&tot)[MT][NT]) {
+    const int col = lane & 15, quarter = lane >> 4;
+    const bf16x8_t ones = __builtin_bit_cast(
+        bf16x8_t, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+    const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int b = 0; b < CH; ++b) {
       if (kb + b < kb_end) {
@@ -227,68 +286,56 @@ struct MfmaBody {
 #pragma unroll
         for (int gi = 0; gi < GPB; ++gi) {
           const int gc = b * GPB + gi;
-          f32x4_t acc[MT][NT];
+          f32x4_t acc[MT][NT], accx[MT];
 #pragma unroll
           for (int js = 0; js < SPG; ++js) {
             const int j = gi * SPG + js;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-              const bf16x8_t A = *reinterpret_cast<const bf16x8_t*>(
-                  &lds.x[buf][16 * mt + col][b * kTileK + 32 * j + 8 * quarter]);
+              const bf16x8_t A = __builtin_bit_cast(
+                  bf16x8_t, lds.x[buf][slot(16 * mt + col, b, 4 * j + quarter)]);
 #pragma unroll
               for (int t = 0; t < NT; ++t) {
                 const uint4 bw = make_uint4(pr[t][4 * j], pr[t][4 * j + 1], pr[t][4 * j + 2],
                                             pr[t][4 * j + 3]);
                 const bf16x8_t B = __builtin_bit_cast(bf16x8_t, bw);
-                const f32x4_t cin = (js == 0) ? f32x4_t{0.f, 0.f, 0.f, 0.f} : acc[mt][t];
-                acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B, cin, 0, 0, 0);
+                acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    A, B, js == 0 ? zero : acc[mt][t], 0, 0, 0);
               }
+              accx[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, ones, js == 0 ? zero : accx[mt],
+                                                                 0, 0, 0);
             }
           }
           float sv[NT], cv[NT];
 #pragma unroll
           for (int t = 0; t < NT; ++t) scale_and_offset(wc.s[gc][t], wc.z[gc][t], sv[t], cv[t]);
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const f32x4_t xs =
-                *reinterpret_cast<const f32x4_t*>(&lds.xsum[buf][gc][16 * mt + 4 * quarter][0]);
+          for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const float v = __builtin_fmaf(sv[t], acc[mt][t][r], tot[mt][t][r]);
-                tot[mt][t][r] = __builtin_fmaf(-cv[t], xs[r], v);
+                tot[mt][t][r] = __builtin_fmaf(-cv[t], accx[mt][r], v);
               }
-          }
         }
       }
     }
   }
 };
 
-template <int BITS, int GROUP, int MT, int NT, int CH>
-__global__ __launch_bounds__(kThreadsPerBlock) void k_qgemm_mfma(QArgs a) {
-  using Body = MfmaBody<BITS, GROUP, MT, NT, CH>;
+template <int BITS, int GROUP, int MT, int NT, int CH, int WAVES, int PF>
+__global__ __launch_bounds__(WAVES * kWave) void k_qgemm_mfma(QArgs a) {
+  static_assert(PF % 2 == 0, "the LDS buffer of a chunk follows the ring slot's parity");
+  using Body = MfmaBody<BITS, GROUP, MT, NT, CH, WAVES>;
   __shared__ typename Body::Lds lds;
 
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const int col = lane & 15, quarter = lane >> 4;
   const int ng = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
-  const int nt0 = (ng * kWavesPerBlock + wave) * NT;
-  const int kb_begin = split * a.blocks_per_split;
-  const int kb_end = min(a.KB, kb_begin + a.blocks_per_split);
-  const int nchunks = (kb_end - kb_begin + CH - 1) / CH;
-
-  const uint8_t* wbase[NT];
-  bool tok[NT];
-  int ncol[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    tok[t] = nt0 + t < a.n_tiles;
-    const int ntc = tok[t] ? nt0 + t : 0;
-    wbase[t] = a.qw + static_cast<size_t>(ntc) * a.KB * (256 * BITS) + lane * (4 * BITS);
-    ncol[t] = ntc * kTileN + col;
-  }
+  const int kb0 = split * a.blocks_per_split;
+  const int kb_end = min(a.KB, kb0 + a.blocks_per_split);
+  const int nchunks = (kb_end - kb0 + CH - 1) / CH;
+  const TileSet<BITS, NT> ts(a, (ng * WAVES + wave) * NT, lane);
 
   f32x4_t tot[MT][NT];
 #pragma unroll
@@ -296,31 +343,49 @@ __global__ __launch_bounds__(kThreadsPerBlock) void k_qgemm_mfma(QArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) tot[mt][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  typename Body::W w0, w1;
-  StageRegs<Body::ROWS, CH> xr;
-  load_wchunk<BITS, GROUP>(w0, a, wbase, ncol, kb_begin, kb_end);
-  load_wchunk<BITS, GROUP>(w1, a, wbase, ncol, kb_begin + CH, kb_end);
-  stage_load(xr, a, kb_begin, kb_end);
-  stage_store(lds, 0, xr);
+  // Weights: a ring of PF chunks.  Activations: two register sets, so the copy of
+  // chunk c+2 is in flight while chunk c is consumed and chunk c+1 goes to LDS.
+  typename Body::W w[PF];
+  typename Body::X x0, x1;
+  static_for<PF>([&](auto u) __attribute__((always_inline)) {
+    load_wchunk<BITS, GROUP>(w[u.value], a, ts.wbase, ts.ncol, kb0 + u.value * CH, kb_end);
+  });
+  Body::stage_load(x0, a, kb0, kb_end);
+  Body::stage_load(x1, a, kb0 + CH, kb_end);
+  Body::stage_store(lds, 0, x0);
   __syncthreads();
 
-  // Straight-line loop body (refills and staging loads are unconditional, clamped
-  // past the end of the split) so that every wait on outstanding loads is exact.
-  for (int c = 0; c < nchunks; c += 2) {
-    const int kb = kb_begin + c * CH;
-    stage_load(xr, a, kb + CH, kb_end);
-    Body::compute(w0, lds, 0, kb, kb_end, col, quarter, tot);
-    load_wchunk<BITS, GROUP>(w0, a, wbase, ncol, kb + 2 * CH, kb_end);
-    stage_store(lds, 1, xr);
+  // One chunk: ring slot U holds chunk c+U; the LDS buffer and the activation register
+  // set follow the chunk's parity (PF is even).  REFILL = false in the drain.
+  auto step = [&](auto u, int c, auto refill) __attribute__((always_inline)) {
+    constexpr int U = decltype(u)::value;
+    const int kb = kb0 + (c + U) * CH;
+    if constexpr (U % 2 == 0) {
+      Body::stage_load(x0, a, kb + 2 * CH, kb_end);
+    } else {
+      Body::stage_load(x1, a, kb + 2 * CH, kb_end);
+    }
+    Body::compute(w[U], lds, U & 1, kb, kb_end, lane, tot);
+    if constexpr (decltype(refill)::value)
+      load_wchunk<BITS, GROUP>(w[U], a, ts.wbase, ts.ncol, kb + PF * CH, kb_end);
+    if constexpr (U % 2 == 0) {
+      Body::stage_store(lds, 1, x1);
+    } else {
+      Body::stage_store(lds, 0, x0);
+    }
     __syncthreads();
-    stage_load(xr, a, kb + 2 * CH, kb_end);
-    Body::compute(w1, lds, 1, kb + CH, kb_end, col, quarter, tot);
-    load_wchunk<BITS, GROUP>(w1, a, wbase, ncol, kb + 3 * CH, kb_end);
-    stage_store(lds, 0, xr);
-    __syncthreads();
-  }
+  };
+
+  // Steady state: straight-line body (every load unconditional and clamped) so that
+  // each wait on outstanding loads is exact.  Then drain the last (at most PF)
+  // chunks without further weight loads.
+  int c = 0;
+  for (; c + PF < nchunks; c += PF)
+    static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::true_type{}); });
+  static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::false_type{}); });
 
   // D layout of 16x16 MFMA: lane holds column lane%16, rows 4*(lane/16) + r.
+  const int quarter = lane >> 4;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -328,19 +393,19 @@ __global__ __launch_bounds__(kThreadsPerBlock) void k_qgemm_mfma(QArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = 16 * mt + 4 * quarter + r;
-        if (tok[t] && m < a.M) store_out(a, split, m, ncol[t], tot[mt][t][r]);
+        if (ts.ok[t] && m < a.M) store_out(a, split, m, ts.ncol[t], tot[mt][t][r]);
       }
 }
 
 // ---------------------------------------------------------------------------
-// GEMV kernel (M <= 8).  Workgroup = 4 wavefronts x NT tiles, one k-split.  The
+// GEMV kernel (small M).  Workgroup = WAVES wavefronts x NT tiles, one k-split.  The
 // split's activations (ROWS x kspan bf16) and the per-quarter group sums of x are
 // staged in LDS once; the main loop then streams weights without barriers.  Lane
 // (quarter q, column c) accumulates its 8-k slices of every step with bf16 dot
 // products; the four quarters are summed at the end (cross-row lane exchange).
 // ---------------------------------------------------------------------------
 
-constexpr int kGemvPieces = 8;  // 16-byte activation pieces staged per thread
+constexpr int kGemvSpans = 2;  // 32-k activation spans staged per thread
 
 // Dynamic LDS layout: x [ROWS][kspan + 8] bf16, then xsum [kspan/GROUP][ROWS][4] f32.
 __host__ __device__ constexpr int gemv_x_stride(int kspan) { return kspan + 8; }
@@ -350,12 +415,7 @@ __host__ __device__ constexpr size_t gemv_xsum_offset(int rows, int kspan) {
 size_t gemv_lds_bytes(int rows, int kspan, int group) {
   return gemv_xsum_offset(rows, kspan) + static_cast<size_t>(kspan / group) * rows * 4 * 4;
 }
-int gemv_max_kspan(int rows) { return kThreadsPerBlock * kGemvPieces * 8 / rows; }
-
-__device__ __forceinline__ float dot2_bf16(uint32_t xa, uint32_t wb, float acc) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xa),
-                                         __builtin_bit_cast(bf16x2_t, wb), acc, false);
-}
+int gemv_max_kspan(int rows, int waves) { return waves * kWave * kGemvSpans * 32 / rows; }
 
 template <int BITS, int GROUP, int ROWS, int NT, int CH>
 struct GemvBody {
@@ -419,69 +479,54 @@ struct GemvBody {
   }
 };
 
-template <int BITS, int GROUP, int ROWS, int NT, int CH>
-__global__ __launch_bounds__(kThreadsPerBlock) void k_qgemv(QArgs a) {
+template <int BITS, int GROUP, int ROWS, int NT, int CH, int WAVES, int PF>
+__global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
+  constexpr int THREADS = WAVES * kWave;
   using Body = GemvBody<BITS, GROUP, ROWS, NT, CH>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const int col = lane & 15, quarter = lane >> 4;
+  const int quarter = lane >> 4;
   const int ng = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
-  const int nt0 = (ng * kWavesPerBlock + wave) * NT;
-  const int kb_begin = split * a.blocks_per_split;
-  const int kb_end = min(a.KB, kb_begin + a.blocks_per_split);
-  const int nblk = kb_end - kb_begin;
+  const int kb0 = split * a.blocks_per_split;
+  const int kb_end = min(a.KB, kb0 + a.blocks_per_split);
+  const int nblk = kb_end - kb0;
   const int nchunks = (nblk + CH - 1) / CH;
   const int kspan = a.blocks_per_split * kTileK;
   const int xs = gemv_x_stride(kspan);
   uint16_t* xl = reinterpret_cast<uint16_t*>(smem);
   float* xsum = reinterpret_cast<float*>(smem + gemv_xsum_offset(ROWS, kspan));
-
-  const uint8_t* wbase[NT];
-  bool tok[NT];
-  int ncol[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    tok[t] = nt0 + t < a.n_tiles;
-    const int ntc = tok[t] ? nt0 + t : 0;
-    wbase[t] = a.qw + static_cast<size_t>(ntc) * a.KB * (256 * BITS) + lane * (4 * BITS);
-    ncol[t] = ntc * kTileN + col;
-  }
+  const TileSet<BITS, NT> ts(a, (ng * WAVES + wave) * NT, lane);
 
   // Start the weight stream before staging the activations.
-  typename Body::W w0, w1;
-  load_wchunk<BITS, GROUP>(w0, a, wbase, ncol, kb_begin, kb_end);
-  load_wchunk<BITS, GROUP>(w1, a, wbase, ncol, kb_begin + CH, kb_end);
+  typename Body::W w[PF];
+  static_for<PF>([&](auto u) __attribute__((always_inline)) {
+    load_wchunk<BITS, GROUP>(w[u.value], a, ts.wbase, ts.ncol, kb0 + u.value * CH, kb_end);
+  });
 
-  // Stage x[0..ROWS)[split] (rows past M repeat row M-1 and are never stored).
+  // Stage x[0..ROWS)[split] (rows past M repeat row M-1 and are never stored) and the
+  // per-quarter group sums: piece q of a span is the quarter-q slice of its 32 k.
   {
-    const int p16 = nblk * 16;  // 16-byte pieces per row
-    const int total = ROWS * p16;
-    uint4 v[kGemvPieces];
+    constexpr int SPAN_G = GROUP / 32;
+    const int spans_per_row = nblk * 4;
+    const int total = ROWS * spans_per_row;
+    SpanRegs<kGemvSpans> r;
+    load_spans<kGemvSpans, THREADS>(r, a, kb0, kb_end, spans_per_row, total);
 #pragma unroll
-    for (int p = 0; p < kGemvPieces; ++p) {
-      const int i = min(p * kThreadsPerBlock + static_cast<int>(threadIdx.x), total - 1);
-      const int row = min(i / p16, a.M - 1), c8 = i % p16;
-      v[p] = *reinterpret_cast<const uint4*>(a.x + static_cast<size_t>(row) * a.K +
-                                             static_cast<size_t>(kb_begin) * kTileK + c8 * 8);
-    }
-    constexpr int P8 = GROUP / 8;
+    for (int p = 0; p < kGemvSpans; ++p) {
+      const int i = p * THREADS + threadIdx.x;
+      const int row = i / spans_per_row, sp = i % spans_per_row;
+      float qs[4];
 #pragma unroll
-    for (int p = 0; p < kGemvPieces; ++p) {
-      const int i = p * kThreadsPerBlock + threadIdx.x;
-      const int row = i / p16, c8 = i % p16;
-      if (i < total) *reinterpret_cast<uint4*>(xl + row * xs + c8 * 8) = v[p];
-      float s = ((bf16lo(v[p].x) + bf16hi(v[p].x)) + (bf16lo(v[p].y) + bf16hi(v[p].y))) +
-                ((bf16lo(v[p].z) + bf16hi(v[p].z)) + (bf16lo(v[p].w) + bf16hi(v[p].w)));
-      // quarter q of a group = pieces with c8 % 4 == q; the pieces of one (row,
-      // block) are one aligned 16-lane row
-      if constexpr (GROUP == 128) {
-        s += dpp_f<kDppRowRor4>(s);
-        s += dpp_f<kDppRowRor8>(s);
-      } else {
-        s += __shfl_xor(s, 4);
+      for (int q = 0; q < 4; ++q) qs[q] = span_reduce<SPAN_G>(piece_sum(r.v[p][q], 0.f));
+      if (i < total) {
+        u32x4_t* dst = reinterpret_cast<u32x4_t*>(xl + row * xs + sp * 32);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) dst[q] = r.v[p][q];
+        if (sp % SPAN_G == 0)
+          *reinterpret_cast<float4*>(xsum + ((sp / SPAN_G) * ROWS + row) * 4) =
+              make_float4(qs[0], qs[1], qs[2], qs[3]);
       }
-      if (i < total && (c8 % P8) < 4) xsum[((c8 / P8) * ROWS + row) * 4 + (c8 % 4)] = s;
     }
   }
   __syncthreads();
@@ -492,15 +537,18 @@ __global__ __launch_bounds__(kThreadsPerBlock) void k_qgemv(QArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) tot[m][t] = 0.f;
 
-  // The refills are unconditional (clamped past the end of the split) so that the
-  // loop body is straight-line and every wait on outstanding loads is exact: a
-  // conditional refill would make the compiler wait for all loads in flight.
-  for (int c = 0; c < nchunks; c += 2) {
-    Body::compute(w0, xl, xsum, xs, c * CH, nblk, quarter, tot);
-    load_wchunk<BITS, GROUP>(w0, a, wbase, ncol, kb_begin + (c + 2) * CH, kb_end);
-    Body::compute(w1, xl, xsum, xs, (c + 1) * CH, nblk, quarter, tot);
-    load_wchunk<BITS, GROUP>(w1, a, wbase, ncol, kb_begin + (c + 3) * CH, kb_end);
+  // Steady state with unconditional (clamped) refills, then a load-free drain.
+  int c = 0;
+  for (; c + PF < nchunks; c += PF) {
+    static_for<PF>([&](auto u) __attribute__((always_inline)) {
+      constexpr int U = decltype(u)::value;
+      Body::compute(w[U], xl, xsum, xs, (c + U) * CH, nblk, quarter, tot);
+      load_wchunk<BITS, GROUP>(w[U], a, ts.wbase, ts.ncol, kb0 + (c + U + PF) * CH, kb_end);
+    });
   }
+  static_for<PF>([&](auto u) __attribute__((always_inline)) {
+    Body::compute(w[decltype(u)::value], xl, xsum, xs, (c + decltype(u)::value) * CH, nblk, quarter, tot);
+  });
 
   // Split-K inside the wavefront: the four quarters hold partial sums of the same
   // column over disjoint k; add the partner rows (lane ^ 16, then lane ^ 32).
@@ -517,7 +565,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void k_qgemv(QArgs a) {
   for (int m = 0; m < ROWS; ++m)
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-      if (tok[t] && (m & 3) == quarter && m < a.M) store_out(a, split, m, ncol[t], tot[m][t]);
+      if (ts.ok[t] && (m & 3) == quarter && m < a.M) store_out(a, split, m, ts.ncol[t], tot[m][t]);
 }
 
 // ---------------------------------------------------------------------------
@@ -527,29 +575,30 @@ __global__ __launch_bounds__(kThreadsPerBlock) void k_qgemv(QArgs a) {
 typedef void (*QKernel)(QArgs);
 
 struct Variant {
-  int path, rows, nt, chunk, bits, group;
+  int path, rows, nt, chunk, waves, prefetch, bits, group;
   QKernel fn;
 };
 
-#define SUBSPEC_GEMV(B, G, R, T, C) {1, R, T, C, B, G, k_qgemv<B, G, R, T, C>}
-#define SUBSPEC_MFMA(B, G, MT, T, C) {2, 16 * MT, T, C, B, G, k_qgemm_mfma<B, G, MT, T, C>}
-#define SUBSPEC_BG(X)                                                                    \
-  X(4, 128) X(4, 64) X(3, 128) X(3, 64) X(2, 128) X(2, 64)
-#define SUBSPEC_GEMV_SET(B, G)                                                          \
-  SUBSPEC_GEMV(B, G, 1, 1, 4), SUBSPEC_GEMV(B, G, 2, 1, 4), SUBSPEC_GEMV(B, G, 4, 1, 4), \
-      SUBSPEC_GEMV(B, G, 8, 1, 4), SUBSPEC_GEMV(B, G, 1, 2, 4), SUBSPEC_GEMV(B, G, 2, 2, 4), \
-      SUBSPEC_GEMV(B, G, 4, 2, 4), SUBSPEC_GEMV(B, G, 8, 2, 4),
-#define SUBSPEC_MFMA_SET(B, G)                                                          \
-  SUBSPEC_MFMA(B, G, 1, 2, 4), SUBSPEC_MFMA(B, G, 2, 2, 2), SUBSPEC_MFMA(B, G, 4, 2, 2), \
-      SUBSPEC_MFMA(B, G, 8, 2, 1),
+#define SUBSPEC_GEMV(B, G, R, T, C, W, P) {1, R, T, C, W, P, B, G, k_qgemv<B, G, R, T, C, W, P>}
+#define SUBSPEC_MFMA(B, G, MT, T, C, W, P) \
+  {2, 16 * MT, T, C, W, P, B, G, k_qgemm_mfma<B, G, MT, T, C, W, P>}
+#define SUBSPEC_BG(X) X(4, 128) X(4, 64) X(3, 128) X(3, 64) X(2, 128) X(2, 64)
+#define SUBSPEC_GEMV_SET(B, G)                                                                \
+  SUBSPEC_GEMV(B, G, 1, 1, 4, 4, 4), SUBSPEC_GEMV(B, G, 2, 1, 4, 4, 4),                       \
+      SUBSPEC_GEMV(B, G, 4, 1, 4, 4, 2), SUBSPEC_GEMV(B, G, 8, 1, 4, 4, 2),
+#define SUBSPEC_MFMA_SET(B, G)                                                                \
+  SUBSPEC_MFMA(B, G, 1, 1, 4, 4, 2), SUBSPEC_MFMA(B, G, 2, 1, 2, 4, 2),                       \
+      SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 4), SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2),                   \
+      SUBSPEC_MFMA(B, G, 1, 2, 4, 4, 2), SUBSPEC_MFMA(B, G, 2, 2, 2, 4, 2),                   \
+      SUBSPEC_MFMA(B, G, 4, 2, 1, 4, 4), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),
 
 static const Variant kVariants[] = {SUBSPEC_BG(SUBSPEC_GEMV_SET) SUBSPEC_BG(SUBSPEC_MFMA_SET)};
 
-static QKernel find_variant(const KernelChoice& kc, int bits, int group) {
+static const Variant* find_variant(const KernelChoice& kc, int bits, int group) {
   for (const Variant& v : kVariants)
     if (v.path == kc.path && v.rows == kc.rows && v.nt == kc.nt && v.chunk == kc.chunk &&
-        v.bits == bits && v.group == group)
-      return v.fn;
+        v.waves == kc.waves && v.bits == bits && v.group == group)
+      return &v;
   return nullptr;
 }
 
@@ -557,12 +606,24 @@ bool qlinear_variant_exists(const KernelChoice& kc, int bits, int group) {
   return find_variant(kc, bits, group) != nullptr;
 }
 
+int qlinear_resident_blocks(const KernelChoice& kc, int bits, int group, size_t dyn_lds) {
+  const Variant* v = find_variant(kc, bits, group);
+  if (!v) return 0;
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(v->fn),
+                                                   kc.waves * kWave, dyn_lds) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return blocks;
+}
+
 hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a, int grid,
                           hipStream_t st) {
-  QKernel fn = find_variant(kc, bits, group);
-  if (!fn) return hipErrorInvalidDeviceFunction;
+  const Variant* v = find_variant(kc, bits, group);
+  if (!v) return hipErrorInvalidDeviceFunction;
   const size_t lds = kc.path == 1 ? gemv_lds_bytes(kc.rows, a.blocks_per_split * kTileK, group) : 0;
-  hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreadsPerBlock), lds, st, a);
+  hipLaunchKernelGGL(v->fn, dim3(grid), dim3(kc.waves * kWave), lds, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   const size_t quads = static_cast<size_t>(a.M) * a.N / 4;

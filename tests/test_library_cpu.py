@@ -99,7 +99,7 @@ def test_plan_choices_are_consistent():
                 KB = K // 128
                 assert p["splits"] >= 1 and p["blocks_per_split"] % p["chunk_blocks"] == 0
                 assert (p["splits"] - 1) * p["blocks_per_split"] < KB <= p["splits"] * p["blocks_per_split"]
-                cols = 4 * p["tiles_per_wave"] * 16
+                cols = p["waves"] * p["tiles_per_wave"] * 16
                 assert p["col_groups"] == -(-N // cols)
                 assert p["grid"] == p["col_groups"] * p["splits"]
                 if p["splits"] == 1:
