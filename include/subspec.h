@@ -151,6 +151,42 @@ int subspec_qdequant(const void* qweight, const void* scales, const void* zeros,
                      int bits, int group, int N, int K, float* w_f32,
                      uint16_t* w_bf16, hipStream_t stream);
 
+/* One projection of a decoder layer for the per-layer launch plan: the draft model
+ * evaluates, per layer, q|k|v (one launch over concatenated columns: they share x),
+ * o, gate|up (concatenated, they share x) and down -- 7 substitute projections in 4
+ * launches.  Concatenating along N is done by the caller before packing (codes
+ * [N1+N2][K], scales and zeros [K/group][N1+N2]); quantization is per column, so the
+ * fused projection is exactly the separate ones side by side. */
+typedef struct subspec_proj {
+  const void* x;        /* device bf16 [M][K]                         */
+  const void* qweight;  /* device, tile layout                        */
+  const void* scales;   /* device fp16 [K/group][N]                   */
+  const void* zeros;    /* device fp16 [K/group][N]                   */
+  void* y;              /* device bf16 [M][N]                         */
+  int N, K;
+} subspec_proj;
+
+/* Run nproj substitute projections in order on `stream` (each one subspec_qlinear;
+ * the automatic plan per shape).  All share bits, group and M. */
+int subspec_stack_forward(const subspec_proj* projs, int nproj, int bits, int group, int M,
+                          hipStream_t stream);
+
+/* A captured launch sequence (HIP graph) of subspec_stack_forward. */
+typedef struct subspec_graph subspec_graph;
+
+/* Capture subspec_stack_forward(projs, ...) on `stream` (which must not be the null
+ * stream) into a graph and instantiate it.  The workspace the sequence needs is
+ * reserved before capture.  The graph keeps the pointers of `projs` (not the array):
+ * replays read and write the same buffers. */
+int subspec_stack_capture(const subspec_proj* projs, int nproj, int bits, int group, int M,
+                          hipStream_t stream, subspec_graph** graph);
+
+/* Replay a captured sequence on `stream` (asynchronous). */
+int subspec_graph_launch(subspec_graph* graph, hipStream_t stream);
+
+/* Release a captured sequence (synchronous with respect to its replays). */
+int subspec_graph_destroy(subspec_graph* graph);
+
 /* Grow the calling device's workspace to at least `bytes` now (synchronous, may
  * call hipMalloc), so that later calls, e.g. under stream capture, need not. */
 int subspec_reserve(size_t bytes);

@@ -22,4 +22,8 @@ from ._binding import (  # noqa: F401
     subspec_qpack_host,
     subspec_quantize,
     subspec_reserve,
+    subspec_stack_forward,
+    subspec_stack_capture,
+    subspec_graph_launch,
+    subspec_graph_destroy,
 )

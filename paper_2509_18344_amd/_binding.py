@@ -31,6 +31,12 @@ class _Plan(ctypes.Structure):
                 ("grid", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t)]
 
 
+class SubspecProj(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("zeros", ctypes.c_void_p), ("y", ctypes.c_void_p), ("N", ctypes.c_int),
+                ("K", ctypes.c_int)]
+
+
 _lib = None
 
 
@@ -59,6 +65,11 @@ def load_library():
         "subspec_qlinear_plan": (I, [I, I, I, I, I, I, ctypes.POINTER(_Plan)]),
         "subspec_qdequant": (I, [P, P, P, I, I, I, I, P, P, P]),
         "subspec_reserve": (I, [S]),
+        "subspec_stack_forward": (I, [ctypes.POINTER(SubspecProj), I, I, I, I, P]),
+        "subspec_stack_capture": (I, [ctypes.POINTER(SubspecProj), I, I, I, I, P,
+                                      ctypes.POINTER(ctypes.c_void_p)]),
+        "subspec_graph_launch": (I, [P, P]),
+        "subspec_graph_destroy": (I, [P]),
         "subspec_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -149,3 +160,36 @@ def subspec_qdequant(qweight, scales, zeros, bits, group, N, K, w_f32, w_bf16,
 
 def subspec_reserve(nbytes: int) -> int:
     return _check("subspec_reserve", load_library().subspec_reserve(nbytes))
+
+
+def _projs(projs):
+    """A ctypes array of subspec_proj from dicts with keys x, qweight, scales, zeros,
+    y, N, K (tensors or addresses)."""
+    arr = (SubspecProj * len(projs))()
+    for i, p in enumerate(projs):
+        arr[i] = SubspecProj(_ptr(p["x"]), _ptr(p["qweight"]), _ptr(p["scales"]), _ptr(p["zeros"]),
+                             _ptr(p["y"]), int(p["N"]), int(p["K"]))
+    return arr
+
+
+def subspec_stack_forward(projs, bits, group, M, stream=None) -> int:
+    arr = _projs(projs)
+    return _check("subspec_stack_forward", load_library().subspec_stack_forward(
+        arr, len(projs), bits, group, M, _stream(stream)))
+
+
+def subspec_stack_capture(projs, bits, group, M, stream) -> int:
+    """Returns the graph handle (an address) of the captured sequence."""
+    arr = _projs(projs)
+    h = ctypes.c_void_p()
+    _check("subspec_stack_capture", load_library().subspec_stack_capture(
+        arr, len(projs), bits, group, M, _stream(stream), ctypes.byref(h)))
+    return h.value
+
+
+def subspec_graph_launch(graph, stream=None) -> int:
+    return _check("subspec_graph_launch", load_library().subspec_graph_launch(graph, _stream(stream)))
+
+
+def subspec_graph_destroy(graph) -> int:
+    return _check("subspec_graph_destroy", load_library().subspec_graph_destroy(graph))

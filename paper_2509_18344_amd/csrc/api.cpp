@@ -392,6 +392,85 @@ int subspec_qdequant(const void* qweight, const void* scales, const void* zeros,
   return SUBSPEC_OK;
 }
 
+int subspec_stack_forward(const subspec_proj* projs, int nproj, int bits, int group, int M,
+                          hipStream_t stream) {
+  if (!projs || nproj < 0) return fail(SUBSPEC_EINVAL, "bad projection list");
+  for (int i = 0; i < nproj; ++i) {
+    const subspec_proj& p = projs[i];
+    const int rc = qlinear_impl(p.x, p.qweight, p.scales, p.zeros, bits, group, M, p.N, p.K, p.y,
+                                SUBSPEC_PATH_AUTO, stream);
+    if (rc) return rc;
+  }
+  return SUBSPEC_OK;
+}
+
+struct subspec_graph {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
+int subspec_stack_capture(const subspec_proj* projs, int nproj, int bits, int group, int M,
+                          hipStream_t stream, subspec_graph** out) {
+  if (!out) return fail(SUBSPEC_EINVAL, "null graph pointer");
+  *out = nullptr;
+  if (!projs || nproj <= 0) return fail(SUBSPEC_EINVAL, "bad projection list");
+  if (stream == nullptr) return fail(SUBSPEC_EINVAL, "capture needs a non-null stream");
+  // Plan every launch first: argument errors surface before capture, and the
+  // workspace is grown (allocation is not capturable) to the largest need.
+  size_t need = 0;
+  for (int i = 0; i < nproj; ++i) {
+    subspec_plan p;
+    const int rc = make_plan(M, projs[i].N, projs[i].K, bits, group, SUBSPEC_PATH_AUTO, &p, nullptr);
+    if (rc) return rc;
+    need = std::max(need, p.workspace_bytes);
+  }
+  if (need) {
+    void* ws = nullptr;
+    const int rc = get_workspace(need, nullptr, &ws);
+    if (rc) return rc;
+  }
+  hipError_t e = hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamBeginCapture");
+  const int rc = subspec_stack_forward(projs, nproj, bits, group, M, stream);
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(stream, &graph);
+  if (rc) {
+    if (graph) hipGraphDestroy(graph);
+    return rc;
+  }
+  if (e != hipSuccess) return hip_fail(e, "hipStreamEndCapture");
+  hipGraphExec_t exec = nullptr;
+  e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  if (e != hipSuccess) {
+    hipGraphDestroy(graph);
+    return hip_fail(e, "hipGraphInstantiate");
+  }
+  subspec_graph* g = new subspec_graph;
+  g->graph = graph;
+  g->exec = exec;
+  *out = g;
+  return SUBSPEC_OK;
+}
+
+int subspec_graph_launch(subspec_graph* g, hipStream_t stream) {
+  if (!g || !g->exec) return fail(SUBSPEC_EINVAL, "null graph");
+  hipError_t e = hipGraphLaunch(g->exec, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipGraphLaunch");
+  return SUBSPEC_OK;
+}
+
+int subspec_graph_destroy(subspec_graph* g) {
+  if (!g) return SUBSPEC_OK;
+  hipError_t e1 = hipDeviceSynchronize();
+  hipError_t e2 = g->exec ? hipGraphExecDestroy(g->exec) : hipSuccess;
+  hipError_t e3 = g->graph ? hipGraphDestroy(g->graph) : hipSuccess;
+  delete g;
+  if (e1 != hipSuccess) return hip_fail(e1, "hipDeviceSynchronize");
+  if (e2 != hipSuccess) return hip_fail(e2, "hipGraphExecDestroy");
+  if (e3 != hipSuccess) return hip_fail(e3, "hipGraphDestroy");
+  return SUBSPEC_OK;
+}
+
 int subspec_reserve(size_t bytes) {
   void* p = nullptr;
   return get_workspace(bytes, nullptr, &p);

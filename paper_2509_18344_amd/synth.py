@@ -57,3 +57,10 @@ def bf16_bits(t) -> np.ndarray:
     """uint16 bit patterns of a (CPU) bfloat16 tensor."""
     import torch
     return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def layer_weights(projs, cfg: int, layer: int, device="cuda"):
+    """fp32 weights of one decoder layer: {name: [N][K]} for the 7 projections, each
+    from its own seeded stream (cfg, layer, projection index)."""
+    return {p.name: weights_torch(p.N, p.K, cfg, layer, i, device=device)
+            for i, p in enumerate(projs)}
