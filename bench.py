@@ -7,22 +7,41 @@ activations, at draft-tree batches M in {1, 8, 32, 64}.  One step = both launche
 at every M (8 launches).  Weights are rotated over enough distinct packed copies
 (>= 1 GB) that no launch finds its weights in the 256 MB last-level cache.
 
+The K timed steps run back to back on one stream between two HIP events (eager
+launches; ``--graph`` replays captured HIP graphs instead).  A second, separate
+pass brackets every launch with events to time each kernel on its own; the
+dominant kernel's roofline comes from that pass.  ``--workload
+qwen7b_stack|qwen32b_stack|qwen32b_2bit`` times whole substitute stacks (all
+layers, 4 launches per layer) captured as one HIP graph per M.
+
 Prints one JSON line: effective weight GB/s (codes + scales + zeros bytes / time)
 of the whole step, the dominant kernel's roofline and the CPU oracle's rate on a
-bounded sample.  ``--workload`` selects another workload for exploration.
+bounded sample.
+
+``--summarize-pmc FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR`` turns four
+rocprofv3 ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` runs (of this script and of its
+``--copy-calibration-mb`` copy) into profiles/traffic.json, which later runs read
+for ``roofline.traffic`` while the kernel sources are unchanged.
 """
 from __future__ import annotations
 
 import argparse
+import collections
+import csv
+import hashlib
 import json
+import math
 import os
+import re
 import sys
 import time
 
 import numpy as np
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def parse():
@@ -34,101 +53,392 @@ def parse():
     ap.add_argument("--ms", default=None, help="comma-separated M values (default: the workload's)")
     ap.add_argument("--rotate-gb", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-cols", type=int, default=1 << 30)
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 GEMV, 2 MFMA")
+    ap.add_argument("--graph", action="store_true",
+                    help="time HIP-graph replays of the step instead of eager launches")
+    ap.add_argument("--per-launch-reps", type=int, default=20)
     ap.add_argument("--json-out", default=None)
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (reference "
                          "for the HBM traffic counters) and exit")
+    ap.add_argument("--summarize-trace", default=None, metavar="TRACE_DIR",
+                    help="print a markdown table of a rocprofv3 --kernel-trace run's "
+                         "library kernels per (kernel, grid) and exit")
+    ap.add_argument("--summarize-pmc", nargs=4, default=None,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"))
     return ap.parse_args()
 
 
-def build_launches(wl, ms, rotate_gb, torch, ss, synth, helpers_quant):
-    """Distinct packed weight copies and per-M activations/outputs."""
-    from paper_2509_18344_amd.workloads import fused_layer, weight_bytes
-    projs = fused_layer(wl.projs) if wl.fused else wl.projs
-    if wl.key == "qwen7b_mlp":  # gate|up share x: one fused launch, like the layer plan
-        projs = (type(projs[0])("gate_up", 3584, 2 * 18944), projs[2])
-    per_copy = sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in projs)
-    copies = max(1, int(np.ceil(rotate_gb * 1e9 / per_copy)))
-    weights = []
-    for c in range(copies):
-        wc = []
-        for pi, p in enumerate(projs):
-            w = synth.weights_torch(p.N, p.K, 11, c, pi, device="cuda")
-            wc.append(helpers_quant(w, wl.bits, wl.group))
-            del w
-        weights.append(wc)
-    torch.cuda.synchronize()
-    acts = {}
-    for M in ms:
-        for pi, p in enumerate(projs):
-            x = synth.activations(M, p.K, 12, M, pi, outlier_frac=wl.outlier_frac).to("cuda")
-            y = torch.empty((M, p.N), dtype=torch.bfloat16, device="cuda")
-            acts[(M, pi)] = (x, y)
-    return projs, weights, acts, per_copy
+# --- kernel identity and measured traffic ----------------------------------------
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("kernels_qlinear.hip", "device_common.h", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2509_18344_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
-def device_quantize(torch, ss):
-    def q(w, bits, group):
-        N, K = w.shape
-        codes = torch.empty((N, K), dtype=torch.uint8, device=w.device)
-        sc = torch.empty((K // group, N), dtype=torch.float16, device=w.device)
-        zr = torch.empty((K // group, N), dtype=torch.float16, device=w.device)
-        ss.subspec_quantize(w, bits, group, N, K, codes, sc, zr)
-        qw = torch.empty(ss.subspec_qpack_bytes(bits, N, K), dtype=torch.uint8, device=w.device)
-        ss.subspec_qpack(codes, bits, N, K, qw)
-        del codes
-        return {"qweight": qw, "scales": sc, "zeros": zr, "N": N, "K": K}
-    return q
+def dispatch_key(family: str, targs, grid_items: int, wg_items: int) -> str:
+    """Kernel identity: template name with its first six arguments (bits, group,
+    rows or row tiles, tiles per wavefront, chunk, wavefronts) and the grid."""
+    return f"{family}<{', '.join(str(a) for a in targs[:6])}> grid={grid_items} wg={wg_items}"
 
 
-def cpu_baseline(wl, sample_cols):
-    """Time the fp64 oracle (unpack + exact dequant + float64 matmul) on one whole
-    projection of the workload at each of its M values; report weight GB/s."""
+def plan_key(plan, bits, group) -> str:
+    wg = plan["waves"] * 64
+    if plan["path"] == 1:
+        family, rows = "k_qgemv", plan["rows"]
+    else:
+        family, rows = "k_qgemm_mfma", plan["rows"] // 16
+    targs = (bits, group, rows, plan["tiles_per_wave"], plan["chunk_blocks"], plan["waves"])
+    return dispatch_key(family, targs, plan["grid"] * wg, wg)
+
+
+def _counter_rows(d, counter):
+    files = [os.path.join(dp, f) for dp, _, fs in os.walk(d) for f in fs
+             if f.endswith("counter_collection.csv")]
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    per = collections.defaultdict(float)
+    meta = {}
+    for fn in files:
+        with open(fn) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] != counter:
+                    continue
+                k = (fn, r["Dispatch_Id"])
+                per[k] += float(r["Counter_Value"])
+                meta[k] = (r["Kernel_Name"], int(r["Grid_Size"]), int(r["Workgroup_Size"]))
+    return [(meta[k][0], meta[k][1], meta[k][2], v) for k, v in per.items()]
+
+
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, calib_bytes=1 << 30):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the qlinear kernels, scaled by
+    what the same counters read for a plain copy of known size."""
+    cf = max(v for (_, _, _, v) in _counter_rows(copy_fetch_dir, "FETCH_SIZE"))
+    cw = max(v for (_, _, _, v) in _counter_rows(copy_write_dir, "WRITE_SIZE"))
+    f_scale = calib_bytes / (cf * 1024.0)
+    w_scale = calib_bytes / (cw * 1024.0)
+    acc = collections.defaultdict(lambda: {"fetch": [], "write": [], "names": set()})
+    for d, which, counter in ((fetch_dir, "fetch", "FETCH_SIZE"), (write_dir, "write", "WRITE_SIZE")):
+        for name, grid, wg, v in _counter_rows(d, counter):
+            m = re.search(r"(k_qgemv|k_qgemm_mfma)<([^>]*)>", name)
+            if not m:
+                continue
+            targs = [int(a) for a in m.group(2).split(",")]
+            e = acc[dispatch_key(m.group(1), targs, grid, wg)]
+            e[which].append(v)
+            e["names"].add(m.group(0))
+    kernels = {}
+    for key, e in sorted(acc.items()):
+        if not e["fetch"] or not e["write"]:
+            continue
+        if len(e["names"]) != 1:  # two template instances share a grid: ambiguous
+            continue
+        fk = float(np.mean(e["fetch"]))
+        wk = float(np.mean(e["write"]))
+        kernels[key] = {"kernel": e["names"].pop(), "dispatches": len(e["fetch"]),
+                        "fetch_kib_raw": round(fk, 1), "write_kib_raw": round(wk, 1),
+                        "hbm_bytes_per_launch": int(round(fk * 1024 * f_scale + wk * 1024 * w_scale))}
+    out = {"kernel_source_sha256_16": kernel_source_hash(),
+           "calibration": {"copy_bytes": calib_bytes, "fetch_kib_raw": cf, "write_kib_raw": cw,
+                           "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
+           "kernels": kernels}
+    os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
+    with open(TRAFFIC_JSON, "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print(json.dumps({"wrote": TRAFFIC_JSON, "kernels": len(kernels),
+                      "fetch_scale": out["calibration"]["fetch_scale"],
+                      "write_scale": out["calibration"]["write_scale"]}))
+
+
+def summarize_trace(d):
+    """Per (kernel, grid) dispatch durations of the library's kernels in a rocprofv3
+    kernel trace, as a markdown table (microseconds)."""
+    files = [os.path.join(dp, f) for dp, _, fs in os.walk(d) for f in fs
+             if f.endswith("kernel_trace.csv")]
+    if not files:
+        raise SystemExit(f"no kernel_trace.csv under {d}")
+    durs = collections.defaultdict(list)
+    for fn in files:
+        with open(fn) as f:
+            for r in csv.DictReader(f):
+                m = re.search(r"(k_\w+)(<[^>]*>)?", r["Kernel_Name"])
+                if not m or "subspec::" not in r["Kernel_Name"]:
+                    continue
+                targs = [int(a) for a in m.group(2)[1:-1].split(",")] if m.group(2) else []
+                name = m.group(1)
+                if name in ("k_qgemv", "k_qgemm_mfma"):
+                    key = dispatch_key(name, targs, int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
+                else:
+                    key = f"{m.group(0)} grid={r['Grid_Size_X']} wg={r['Workgroup_Size_X']}"
+                durs[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    print("| kernel (template args, grid and workgroup in work-items) | dispatches | avg us | median us | min us | max us |")
+    print("|---|---|---|---|---|---|")
+    for key, v in sorted(durs.items()):
+        a = np.array(v)
+        print(f"| `{key}` | {len(a)} | {a.mean():.2f} | {np.median(a):.2f} | {a.min():.2f} | {a.max():.2f} |")
+
+
+def measured_traffic(key: str):
+    """HBM bytes per launch for `key` from profiles/traffic.json, if those counters
+    were taken on the current kernel sources; else None."""
+    try:
+        with open(TRAFFIC_JSON) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if data.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    entry = data.get("kernels", {}).get(key)
+    return None if entry is None else entry.get("hbm_bytes_per_launch")
+
+
+# --- CPU oracle baseline --------------------------------------------------------
+
+def cpu_baseline(wl, ms, min_seconds=10.0):
+    """Time the fp64 oracle (unpack + exact dequant + float64 matmul) on the bench
+    step's own launches (every projection at every M), repeating the step until
+    `min_seconds` have passed; report weight GB/s.  Stacks use one layer."""
     import oracle
     import paper_2509_18344_amd as ss
     from paper_2509_18344_amd import synth
-    from paper_2509_18344_amd.workloads import weight_bytes
+    from paper_2509_18344_amd.workloads import Proj, fused_layer, weight_bytes
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover - threadpoolctl missing
         blas_threads = len(os.sched_getaffinity(0))
-    p = max(wl.projs, key=lambda q: (q.K, q.N))
-    N = min(p.N, sample_cols)
-    K = p.K
-    w = synth.weights_np(N, K, 13)
-    q, s16, z16 = oracle.quantize_minmax(w, wl.bits, wl.group)
-    del w
-    packed = np.zeros(ss.subspec_qpack_bytes(wl.bits, N, K), np.uint8)
-    ss.subspec_qpack_host(q, wl.bits, N, K, packed)
-    xs = {M: synth.bf16_bits(synth.activations(M, K, 14, M)) for M in wl.ms}
+    if wl.key == "qwen7b_mlp":
+        projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
+    elif wl.layers > 1:
+        projs = fused_layer(wl.projs)
+    else:
+        projs = wl.projs
+    prepared = []
+    for pi, p in enumerate(projs):
+        w = synth.weights_np(p.N, p.K, 13, pi)
+        q, s16, z16 = oracle.quantize_minmax(w, wl.bits, wl.group)
+        del w
+        packed = np.zeros(ss.subspec_qpack_bytes(wl.bits, p.N, p.K), np.uint8)
+        ss.subspec_qpack_host(q, wl.bits, p.N, p.K, packed)
+        del q
+        xs = {M: synth.bf16_bits(synth.activations(M, p.K, 14, M, pi, outlier_frac=wl.outlier_frac))
+              for M in ms}
+        prepared.append((p, packed, s16, z16, xs))
     np.ones((64, 64)) @ np.ones((64, 64))  # start the BLAS thread pool outside the timing
+    steps = 0
     t0 = time.perf_counter()
-    for M in wl.ms:
-        codes = oracle.unpack(packed, wl.bits, N, K)
-        y = oracle.qlinear_ref(xs[M], codes, s16, z16, wl.group)
-        assert y.shape == (M, N)
-    dt = time.perf_counter() - t0
-    wb = weight_bytes(N, K, wl.bits, wl.group) * len(wl.ms)
+    while True:
+        for M in ms:
+            for (p, packed, s16, z16, xs) in prepared:
+                codes = oracle.unpack(packed, wl.bits, p.N, p.K)
+                y = oracle.qlinear_ref(xs[M], codes, s16, z16, wl.group)
+                assert y.shape == (M, p.N)
+                del codes, y
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    wb = steps * len(ms) * sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in projs)
+    names = "+".join(f"{p.name}(K={p.K},N={p.N})" for p in projs)
     return {"value": round(wb / dt / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
             "kind": "oracle", "seconds": round(dt, 3),
-            "sample": f"{p.name} projection K={K} N={N} (of {p.N}) at M in {list(wl.ms)}: "
-                      f"unpack + fp64 dequant (one thread) + fp64 BLAS matmul "
-                      f"({blas_threads} threads); {wb / 1e6:.1f} MB of weights"}
+            "sample": f"{steps} pass(es) of {names} at M in {list(ms)}"
+                      f"{' (one layer of the stack)' if wl.layers > 1 else ''}: unpack + fp64 "
+                      f"dequant (one thread) + fp64 BLAS matmul ({blas_threads} threads); "
+                      f"{wb / 1e6:.1f} MB of weights"}
+
+
+# --- GPU timing -------------------------------------------------------------------
+
+def per_launch_stats(torch, ss, wl, items, reps, stream):
+    """Time each (M, proj, argsets) eagerly between events, `reps` times, cycling
+    through its argument sets (distinct weight copies)."""
+    from paper_2509_18344_amd.workloads import weight_bytes
+    out = []
+    for (M, p, argsets) in items:
+        ev = []
+        for r in range(reps):
+            a = argsets[r % len(argsets)]
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            ss.subspec_qlinear(a["x"], a["qweight"], a["scales"], a["zeros"], wl.bits, wl.group,
+                               M, p.N, p.K, a["y"], stream)
+            e1.record(stream)
+            ev.append((e0, e1))
+        torch.cuda.synchronize()
+        t = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3  # us
+        plan = ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group)
+        wb = weight_bytes(p.N, p.K, wl.bits, wl.group)
+        ab = wb + 2 * M * p.K + 2 * M * p.N
+        flops = 2.0 * M * p.N * p.K
+        avg = float(t.mean())
+        out.append({"proj": p.name, "M": M, "N": p.N, "K": p.K, "path": plan["path"],
+                    "key": plan_key(plan, wl.bits, wl.group), "grid": plan["grid"], "splits": plan["splits"],
+                    "avg_us": round(avg, 2), "p10_us": round(float(np.percentile(t, 10)), 2),
+                    "p90_us": round(float(np.percentile(t, 90)), 2),
+                    "weight_GBs": round(wb / (avg * 1e-6) / 1e9, 1),
+                    "alg_GBs": round(ab / (avg * 1e-6) / 1e9, 1),
+                    "TFLOPs": round(flops / (avg * 1e-6) / 1e12, 2),
+                    "alg_bytes": ab, "flops": flops})
+    return out
+
+
+def timed(torch, stream, fn, warmup, steps):
+    for s in range(warmup):
+        fn(s)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for s in range(steps):
+        fn(warmup + s)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1)
+
+
+def run_projections(args, torch, ss, wl, ms, stream):
+    """Independent projections at several M; weights rotate over distinct copies."""
+    from paper_2509_18344_amd import prepare, synth
+    from paper_2509_18344_amd.workloads import Proj, weight_bytes
+    projs = wl.projs
+    if wl.key == "qwen7b_mlp":  # gate|up share x: one fused launch, as in the layer plan
+        projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
+    per_copy = sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in projs)
+    copies = max(1, int(math.ceil(args.rotate_gb * 1e9 / per_copy)))
+    weights = []
+    for c in range(copies):
+        wc = []
+        for pi, p in enumerate(projs):
+            w = synth.weights_torch(p.N, p.K, 11, c, pi, device="cuda")
+            wc.append(prepare.quantize_pack(w, wl.bits, wl.group))
+            del w
+        weights.append(wc)
+    acts = {}
+    for M in ms:
+        for pi, p in enumerate(projs):
+            x = synth.activations(M, p.K, 12, M, pi, outlier_frac=wl.outlier_frac).to("cuda")
+            acts[(M, pi)] = (x, torch.empty((M, p.N), dtype=torch.bfloat16, device="cuda"))
+    torch.cuda.synchronize()
+    launches = [(M, pi) for M in ms for pi in range(len(projs))]
+    nl = len(launches)
+    need = max(ss.subspec_qlinear_plan(M, projs[pi].N, projs[pi].K, wl.bits, wl.group,
+                                       args.path)["workspace_bytes"] for (M, pi) in launches)
+    ss.subspec_reserve(need)
+
+    def proj_dict(s, li):
+        M, pi = launches[li]
+        wc = weights[(s * nl + li) % copies][pi]
+        x, y = acts[(M, pi)]
+        return {"x": x, "y": y, "qweight": wc["qweight"], "scales": wc["scales"],
+                "zeros": wc["zeros"], "N": projs[pi].N, "K": projs[pi].K}
+
+    graphs = []
+    period = copies // math.gcd(copies, nl)
+    if args.graph:
+        for s in range(period):  # one graph per M (the API captures one M at a time)
+            gs = []
+            for M in ms:
+                lst = [proj_dict(s, li) for li in range(nl) if launches[li][0] == M]
+                gs.append(ss.subspec_stack_capture(lst, wl.bits, wl.group, M, stream))
+            graphs.append(gs)
+
+    def step(s):
+        if args.graph:
+            for g in graphs[s % period]:
+                ss.subspec_graph_launch(g, stream)
+            return
+        for li in range(nl):
+            d = proj_dict(s, li)
+            ss.subspec_qlinear_path(d["x"], d["qweight"], d["scales"], d["zeros"], wl.bits,
+                                    wl.group, launches[li][0], d["N"], d["K"], d["y"],
+                                    args.path, stream)
+
+    total_ms = timed(torch, stream, step, args.warmup, args.steps)
+    for gs in graphs:
+        for g in gs:
+            ss.subspec_graph_destroy(g)
+    items = []
+    for (M, pi) in launches:
+        x, y = acts[(M, pi)]
+        items.append((M, projs[pi], [{"x": x, "y": y, **{k: weights[c][pi][k] for k in
+                                                          ("qweight", "scales", "zeros")}}
+                                     for c in range(copies)]))
+    per = per_launch_stats(torch, ss, wl, items, max(args.per_launch_reps, copies), stream)
+    return {"total_ms": total_ms, "per_launch": per, "launches_per_step": nl, "copies": copies,
+            "rotation_GB": round(copies * per_copy / 1e9, 2),
+            "step_bytes": sum(weight_bytes(projs[pi].N, projs[pi].K, wl.bits, wl.group)
+                              for (_, pi) in launches),
+            "step_flops": sum(2.0 * M * projs[pi].N * projs[pi].K for (M, pi) in launches),
+            "timing": "HIP graph replays" if args.graph else "eager launches"}
+
+
+def run_stack(args, torch, ss, wl, ms, stream):
+    """All layers of a substitute stack, 4 launches per layer, one HIP graph per M;
+    one step = one pass of the stack at every M."""
+    from paper_2509_18344_amd import prepare, synth
+    from paper_2509_18344_amd.workloads import fused_layer, weight_bytes
+    plan = fused_layer(wl.projs)
+    packed = []
+    for l in range(wl.layers):
+        w = synth.layer_weights(wl.projs, 20, l)
+        parts = [[w["q"], w["k"], w["v"]], [w["o"]], [w["gate"], w["up"]], [w["down"]]]
+        packed.append([prepare.fused(ps, wl.bits, wl.group) if len(ps) > 1 else
+                       prepare.quantize_pack(ps[0], wl.bits, wl.group) for ps in parts])
+        del w
+    torch.cuda.synchronize()
+    xs, ys, graphs = {}, {}, []
+    for M in ms:
+        xs[M] = [[synth.activations(M, p.K, 21, l, li, outlier_frac=wl.outlier_frac).to("cuda")
+                  for li, p in enumerate(plan)] for l in range(wl.layers)]
+        ys[M] = [[torch.empty((M, p.N), dtype=torch.bfloat16, device="cuda") for p in plan]
+                 for _ in range(wl.layers)]
+        launches = []
+        for l in range(wl.layers):
+            launches += prepare.layer_launches(packed[l], xs[M][l], ys[M][l])
+        graphs.append(ss.subspec_stack_capture(launches, wl.bits, wl.group, M, stream))
+
+    def step(s):
+        for g in graphs:
+            ss.subspec_graph_launch(g, stream)
+
+    total_ms = timed(torch, stream, step, args.warmup, args.steps)
+    for g in graphs:
+        ss.subspec_graph_destroy(g)
+    per = []
+    for M in ms:
+        items = [(M, p, [{"x": xs[M][l][li], "y": ys[M][l][li],
+                          **{k: packed[l][li][k] for k in ("qweight", "scales", "zeros")}}
+                         for l in range(wl.layers)]) for li, p in enumerate(plan)]
+        per += per_launch_stats(torch, ss, wl, items, wl.layers, stream)
+    layer_bytes = sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in plan)
+    return {"total_ms": total_ms, "per_launch": per, "launches_per_step": 4 * wl.layers * len(ms),
+            "copies": 1, "rotation_GB": round(layer_bytes * wl.layers / 1e9, 2),
+            "step_bytes": layer_bytes * wl.layers * len(ms),
+            "step_flops": sum(wl.layers * 2.0 * M * p.N * p.K for M in ms for p in plan),
+            "timing": "HIP graph replays"}
 
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the library has no "
               "multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2509_18344_amd as ss
-    from paper_2509_18344_amd import synth
-    from paper_2509_18344_amd.workloads import WORKLOADS, weight_bytes
+    from paper_2509_18344_amd.workloads import WORKLOADS
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -145,88 +455,32 @@ def main():
     ss.load_library()
     wl = WORKLOADS[args.workload]
     ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else wl.ms
+    stream = torch.cuda.Stream()
     t_setup = time.perf_counter()
-    projs, weights, acts, per_copy = build_launches(wl, ms, args.rotate_gb, torch, ss, synth,
-                                                    device_quantize(torch, ss))
-    # Reserve the split-K workspace up front so no launch allocates.
-    need = 0
-    for M in ms:
-        for p in projs:
-            need = max(need, ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group,
-                                                     args.path)["workspace_bytes"])
-    ss.subspec_reserve(need)
-    torch.cuda.synchronize()
-    setup_s = time.perf_counter() - t_setup
+    with torch.cuda.stream(stream):
+        if wl.layers > 1:
+            r = run_stack(args, torch, ss, wl, ms, stream)
+        else:
+            r = run_projections(args, torch, ss, wl, ms, stream)
+    wall_s = time.perf_counter() - t_setup
 
-    launches = [(M, pi) for M in ms for pi in range(len(projs))]
-    copies = len(weights)
-    stream = torch.cuda.current_stream()
-    counter = [0]
-
-    def step(events=None):
-        for li, (M, pi) in enumerate(launches):
-            wc = weights[counter[0] % copies][pi]
-            counter[0] += 1
-            x, y = acts[(M, pi)]
-            p = projs[pi]
-            if events is not None:
-                events[li][0].record(stream)
-            ss.subspec_qlinear_path(x, wc["qweight"], wc["scales"], wc["zeros"], wl.bits,
-                                    wl.group, M, p.N, p.K, y, args.path, stream.cuda_stream)
-            if events is not None:
-                events[li][1].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    per_launch = {li: [] for li in range(len(launches))}
-    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-           for _ in launches] for _ in range(args.steps)]
-    t_all0 = torch.cuda.Event(enable_timing=True)
-    t_all1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_all0.record(stream)
-    for s in range(args.steps):
-        step(ev[s])
-    t_all1.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_all0.elapsed_time(t_all1)
-    for s in range(args.steps):
-        for li in range(len(launches)):
-            per_launch[li].append(ev[s][li][0].elapsed_time(ev[s][li][1]))
-
-    step_weight_bytes = sum(weight_bytes(projs[pi].N, projs[pi].K, wl.bits, wl.group)
-                            for (_, pi) in launches)
-    ms_per_step = total_ms / args.steps
-    value = step_weight_bytes / (ms_per_step * 1e-3) / 1e9
-
-    detail = []
-    best = None
-    for li, (M, pi) in enumerate(launches):
-        p = projs[pi]
-        t = np.array(per_launch[li])
-        avg_us = float(t.mean() * 1e3)
-        wb = weight_bytes(p.N, p.K, wl.bits, wl.group)
-        ab = wb + 2 * M * p.K + 2 * M * p.N
-        flops = 2.0 * M * p.N * p.K
-        plan = ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group, args.path)
-        d = {"proj": p.name, "M": M, "N": p.N, "K": p.K, "path": plan["path"],
-             "grid": plan["grid"], "splits": plan["splits"], "avg_us": round(avg_us, 2),
-             "p10_us": round(float(np.percentile(t, 10) * 1e3), 2),
-             "p90_us": round(float(np.percentile(t, 90) * 1e3), 2),
-             "weight_GBs": round(wb / (avg_us * 1e-6) / 1e9, 1),
-             "alg_GBs": round(ab / (avg_us * 1e-6) / 1e9, 1),
-             "TFLOPs": round(flops / (avg_us * 1e-6) / 1e12, 2),
-             "total_ms": float(t.sum())}
-        detail.append(d)
-        if best is None or d["total_ms"] > best["total_ms"]:
-            best = d | {"alg_bytes": ab, "flops": flops}
-    peak_frac_hbm = best["alg_GBs"] / HBM_PEAK_GBS
-    roofline = {"bound": "hbm", "achieved": best["alg_GBs"], "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(peak_frac_hbm, 4), "traffic": None,
-                "kernel": f"{'k_qgemv' if best['path'] == 1 else 'k_qgemm_mfma'} "
-                          f"{best['proj']} M={best['M']} N={best['N']} K={best['K']}",
-                "alg_bytes_per_launch": best["alg_bytes"], "avg_us": best["avg_us"]}
+    ms_per_step = r["total_ms"] / args.steps
+    value = r["step_bytes"] / (ms_per_step * 1e-3) / 1e9
+    per = r["per_launch"]
+    # dominant kernel: the launch with the largest share of the step's kernel time
+    dom = max(per, key=lambda d: d["avg_us"])
+    ridge = (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9)
+    if dom["flops"] / dom["alg_bytes"] > ridge:
+        roofline = {"bound": "mfma", "achieved": dom["TFLOPs"], "peak": MFMA_BF16_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(dom["TFLOPs"] / MFMA_BF16_PEAK_TFLOPS, 4)}
+    else:
+        roofline = {"bound": "hbm", "achieved": dom["alg_GBs"], "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(dom["alg_GBs"] / HBM_PEAK_GBS, 4)}
+    roofline.update({"traffic": measured_traffic(dom["key"]),
+                     "kernel": f"{dom['key']} ({dom['proj']} M={dom['M']} N={dom['N']} K={dom['K']})",
+                     "avg_us": dom["avg_us"], "alg_bytes_per_launch": dom["alg_bytes"],
+                     "flops_per_launch": dom["flops"],
+                     "kernel_source_sha256_16": kernel_source_hash()})
 
     out = {
         "metric": "effective weight GB/s and % HBM roofline of low-bit qlinear at draft-tree M",
@@ -243,17 +497,19 @@ def main():
         "data": "synthetic: N(0,0.02) fp32 weights min/max-quantized on the GPU, N(0,1) bf16 "
                 "activations, seeded",
         "config": {"workload": wl.description, "bits": wl.bits, "group": wl.group,
-                   "ms": list(ms), "launches_per_step": len(launches),
-                   "weight_bytes_per_step": step_weight_bytes,
-                   "distinct_weight_copies": copies,
-                   "rotation_GB": round(copies * per_copy / 1e9, 2),
-                   "hbm_fraction_of_8TBs": round(value / HBM_PEAK_GBS, 4)},
+                   "ms": list(ms), "layers": wl.layers,
+                   "launches_per_step": r["launches_per_step"],
+                   "weight_bytes_per_step": r["step_bytes"],
+                   "distinct_weight_copies": r["copies"], "rotation_GB": r["rotation_GB"],
+                   "timing": r["timing"],
+                   "hbm_fraction_of_8TBs": round(value / HBM_PEAK_GBS, 4),
+                   "TFLOPs": round(r["step_flops"] / (ms_per_step * 1e-3) / 1e12, 2)},
         "roofline": roofline,
-        "per_launch": [{k: v for k, v in d.items() if k != "total_ms"} for d in detail],
-        "setup_s": round(setup_s, 2),
+        "per_launch": [{k: v for k, v in d.items() if k not in ("alg_bytes", "flops")} for d in per],
+        "wall_s": round(wall_s, 2),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_cols)
+        out["cpu_baseline"] = cpu_baseline(wl, ms)
     line = json.dumps(out)
     if args.json_out:
         with open(args.json_out, "w") as f:

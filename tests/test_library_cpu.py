@@ -106,7 +106,9 @@ def test_plan_choices_are_consistent():
                     assert p["workspace_bytes"] == 0
                 else:
                     assert p["workspace_bytes"] == p["splits"] * M * N * 4
-    assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_GEMV
+    assert ss.subspec_qlinear_plan(2, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_GEMV
+    assert ss.subspec_qlinear_plan(3, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_MFMA
+    assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_GEMV)["path"] == ss.SUBSPEC_PATH_GEMV
     assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_MFMA)["path"] == ss.SUBSPEC_PATH_MFMA
 
 
