@@ -86,7 +86,8 @@ typedef struct subspec_plan {
   int splits;          /* workgroups along K (split-K); 1 = no partial results    */
   int blocks_per_split;/* 128-k blocks per split                                  */
   int grid;            /* total workgroups = col_groups * splits                  */
-  size_t workspace_bytes; /* device scratch needed: fp32 partial sums of the splits */
+  size_t workspace_bytes; /* device scratch needed when splits > 1: 64 KiB of
+                             completion counters + the splits' fp32 partial sums */
 } subspec_plan;
 
 /* Bytes of the packed code buffer for an N x K projection.  0 on bad arguments. */

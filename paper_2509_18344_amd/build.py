@@ -17,6 +17,9 @@ HIPCC_FLAGS = [
     "-ffp-contract=off",
     # keep the compiler from emitting packed fp32 VALU instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the per-group scale/offset FMAs
+    # read them directly instead of copying them out of AGPRs first
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wno-unused-command-line-argument",
 ]
 

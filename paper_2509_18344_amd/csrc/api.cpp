@@ -46,8 +46,10 @@ int check_tiles(int N, int K) {
   if (N <= 0 || K <= 0) return fail(SUBSPEC_EINVAL, "N=%d, K=%d: must be positive", N, K);
   if (N % subspec::kTileN) return fail(SUBSPEC_EUNSUPPORTED, "N=%d: must be a multiple of 16", N);
   if (K % subspec::kTileK) return fail(SUBSPEC_EUNSUPPORTED, "K=%d: must be a multiple of 128", K);
-  if (static_cast<long long>(N) * K > (1ll << 40))
-    return fail(SUBSPEC_EUNSUPPORTED, "N*K=%lld too large", static_cast<long long>(N) * K);
+  // The kernels address every operand with 32-bit byte offsets.
+  if (static_cast<long long>(N) * K > (1ll << 32))
+    return fail(SUBSPEC_EUNSUPPORTED, "N*K=%lld too large (at most 2^32)", static_cast<long long>(N) * K);
+  if (K > (1 << 24)) return fail(SUBSPEC_EUNSUPPORTED, "K=%d too large (at most 2^24)", K);
   return SUBSPEC_OK;
 }
 
@@ -63,7 +65,7 @@ struct Tuning {
   int gemv_max_m = kAutoGemvMaxRows;  // largest M the automatic plan sends to the GEMV path
   int target_blocks = 0;          // workgroups to aim for; 0 = one full residency round
   int gemv_nt = 1;
-  int mfma_nt = 1;                // tiles per MFMA wavefront; 0 = choose per shape
+  int mfma_nt = 0;                // tiles per MFMA wavefront; 0 = choose per shape
   int splits = 0;                 // 0 = choose per shape
   int partial_div = 2;            // split-K partial traffic may reach weight bytes / this
 };
@@ -138,9 +140,9 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c.rows = 16 * mt;
     // LDS holds two chunks of rows x (128*chunk) activations: ~34 KB up to M = 64.
     c.chunk = mt == 1 ? 4 : mt == 2 ? 2 : 1;
-    // Two tiles per wavefront halve the activation reads from LDS; one tile per
-    // wavefront doubles the workgroups for narrow projections.
-    c.nt = tu.mfma_nt ? tu.mfma_nt : ((n_tiles / 8) >= device_cus() ? 2 : 1);
+    // From 64 rows on, two tiles per wavefront halve the activation reads from LDS
+    // (the A fragments are shared by the wavefront's tiles).
+    c.nt = tu.mfma_nt ? tu.mfma_nt : (mt >= 4 ? 2 : 1);
   } else {
     return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
   }
@@ -176,6 +178,12 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     const int min_splits = (chunks + max_chunks - 1) / max_chunks;
     if (splits < min_splits) splits = min_splits;
   }
+  // Split-K needs a completion counter per column group and 32-bit offsets into the
+  // partial sums.
+  if (col_groups > subspec::kSplitCounters) splits = 1;
+  const long long split_bytes = 4ll * M * N;
+  if (splits > 1 && split_bytes * splits >= (1ll << 31))
+    splits = std::max(1, static_cast<int>(((1ll << 31) - 1) / split_bytes));
   if (splits > chunks) splits = chunks;
   int chunks_per_split = (chunks + splits - 1) / splits;
   const int blocks_per_split = chunks_per_split * c.chunk;
@@ -190,7 +198,8 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   p->blocks_per_split = blocks_per_split;
   p->grid = col_groups * splits;
   p->workspace_bytes = 0;
-  if (splits > 1) p->workspace_bytes = static_cast<size_t>(splits) * M * N * sizeof(float);
+  if (splits > 1)
+    p->workspace_bytes = subspec::kSplitCounterBytes + static_cast<size_t>(splits) * M * N * sizeof(float);
   if (kc) *kc = c;
   return SUBSPEC_OK;
 }
@@ -244,6 +253,13 @@ int get_workspace(size_t bytes, hipStream_t st, void** out) {
   void* p = nullptr;
   e = hipMalloc(&p, nb);
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
+  // The split-K completion counters start at zero; every launch leaves them at zero.
+  e = hipMemset(p, 0, subspec::kSplitCounterBytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    (void)hipFree(p);
+    return hip_fail(e, "hipMemset(workspace counters)");
+  }
   w.ptr = p;
   w.bytes = nb;
   *out = p;
@@ -314,7 +330,8 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
     void* ws = nullptr;
     rc = get_workspace(p.workspace_bytes, st, &ws);
     if (rc) return rc;
-    a.ws = static_cast<float*>(ws);
+    a.cnt = static_cast<unsigned*>(ws);
+    a.ws = reinterpret_cast<float*>(static_cast<char*>(ws) + subspec::kSplitCounterBytes);
   }
   hipError_t e = subspec::launch_qlinear(kc, bits, group, a, p.grid, st);
   if (e != hipSuccess) return hip_fail(e, "qlinear launch");

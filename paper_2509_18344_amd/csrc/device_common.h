@@ -44,6 +44,31 @@ __device__ __forceinline__ Slice<BITS> load_slice(const uint8_t* __restrict__ p)
   return s;
 }
 
+// Raw buffer resource over `bytes` bytes at p (32-bit offsets from one scalar base,
+// so address arithmetic stays in 32 bits).  Word 3 selects the 32-bit data format
+// raw buffer accesses need on CDNA; loads at offsets past `bytes` return zeros.
+constexpr int kBufferWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, static_cast<int>(bytes),
+                                           kBufferWord3);
+}
+
+template <int BITS>
+__device__ __forceinline__ Slice<BITS> load_slice(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  Slice<BITS> s;
+  if constexpr (BITS == 4) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    s.w[0] = v[0]; s.w[1] = v[1]; s.w[2] = v[2]; s.w[3] = v[3];
+  } else if constexpr (BITS == 2) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    s.w[0] = v[0]; s.w[1] = v[1];
+  } else {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b96(r, off, 0, 0);
+    s.w[0] = v[0]; s.w[1] = v[1]; s.w[2] = v[2];
+  }
+  return s;
+}
+
 // (a & mask) | bias in one VALU instruction: gfx950's three-input bitwise
 // v_bitop3_b32 with truth table 0xEA (inputs weighted 0xF0, 0xCC, 0xAA).  Through
 // the builtin, not inline assembly, so the compiler sees the instruction and keeps

@@ -20,6 +20,7 @@ struct QArgs {
   const uint16_t* zr;     // fp16 [K/group][N]
   uint16_t* y;            // bf16 [M][N]
   float* ws;              // fp32 [splits][M][N] partial sums (splits > 1)
+  unsigned* cnt;          // per column group: workgroups done (zero between launches)
   int M, N, K;
   int KB;                 // K / 128
   int n_tiles;            // N / 16
@@ -51,6 +52,8 @@ hipError_t launch_qpack(const uint8_t* codes, int bits, int N, int K, void* qw, 
 hipError_t launch_qdequant(const void* qw, const void* sc, const void* zr, int bits, int group,
                            int N, int K, float* wf, uint16_t* wb, hipStream_t st);
 
-constexpr int kThreadsPerBlock = 256;  // split-K reduction kernel
+// Split-K workspace: kSplitCounters zeroed counters, then the fp32 partial sums.
+constexpr int kSplitCounters = 16384;
+constexpr size_t kSplitCounterBytes = kSplitCounters * sizeof(unsigned);
 
 }  // namespace subspec

@@ -8,7 +8,8 @@
 //                 from LDS, the B operand straight from the unpacked codes.
 //
 // Both split K across workgroups when a projection has too few columns to fill the
-// GPU; the fp32 partial sums are then added in split order by k_splitk_reduce.
+// GPU; the last workgroup of a column group to finish adds the fp32 partial sums in
+// split order (finish_splitk).
 //
 // Dequantization is folded into the accumulation.  Within one group the weight is
 // affine in the code, W^ = s*(q - z), so for every (row m, column n, group g)
@@ -156,36 +157,67 @@ __device__ __forceinline__ void scale_and_offset(uint32_t sbits, uint32_t zbits,
 }
 
 // ---------------------------------------------------------------------------
-// Output: with one split the result goes straight to y; otherwise each workgroup
-// stores fp32 partial sums and k_splitk_reduce (launched next on the same stream,
-// so the kernel boundary orders the two) adds them in split order.
+// Output.  With one split the result goes straight to y.  Otherwise every workgroup
+// stores fp32 partial sums ws[split][m][n], and the last workgroup of its column
+// group to finish adds them in split order and writes y (finish_splitk).  The
+// partial sums are written and read with agent-scope cache policy (coherent across
+// the XCDs' L2 caches) and each workgroup waits for its own stores before counting
+// itself in, so no cache flush or invalidation is needed.
 // ---------------------------------------------------------------------------
+
+constexpr int kCachePolicyAgent = 16;  // sc1: coherent at agent scope
+// s_waitcnt vmcnt(0), other counters untouched (expcnt 7, lgkmcnt 15).
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 __device__ __forceinline__ void store_out(const QArgs& a, int split, int m, int n, float v) {
   if (a.splits == 1)
     a.y[static_cast<size_t>(m) * a.N + n] = float_to_bf16_bits(v);
   else
-    a.ws[(static_cast<size_t>(split) * a.M + m) * a.N + n] = v;
+    __hip_atomic_store(a.ws + (static_cast<size_t>(split) * a.M + m) * a.N + n, v, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// y[m][n] = bf16(sum over s of ws[s][m][n]), s ascending; 4 columns per thread.
-__global__ __launch_bounds__(kThreadsPerBlock) void k_splitk_reduce(const float* __restrict__ ws,
-                                                                     uint16_t* __restrict__ y,
-                                                                     int M, int N, int splits) {
-  const size_t quads = static_cast<size_t>(M) * N / 4;
-  const size_t i = static_cast<size_t>(blockIdx.x) * kThreadsPerBlock + threadIdx.x;
-  if (i >= quads) return;
-  const float4* src = reinterpret_cast<const float4*>(ws) + i;
-  float4 acc = src[0];
-  for (int sp = 1; sp < splits; ++sp) {
-    const float4 v = src[sp * quads];
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+// Split-K completion for column group ng (columns [ng*cols, ng*cols + cols) of N):
+// called by every thread of the workgroup after its partial sums are stored.
+template <int THREADS>
+__device__ __forceinline__ void finish_splitk(const QArgs& a, int ng, int cols) {
+  __shared__ int last;
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __syncthreads();
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(a.cnt + ng, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+           static_cast<unsigned>(a.splits - 1);
+  __syncthreads();
+  if (!last) return;
+  const int n0 = ng * cols;
+  const int nq = min(cols, a.N - n0) / 4;  // column quads of the group
+  const uint32_t split_bytes = static_cast<uint32_t>(a.M) * a.N * 4;
+  const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(a.ws, split_bytes * a.splits);
+  for (int q = threadIdx.x; q < a.M * nq; q += THREADS) {
+    const int m = q / nq, n = n0 + 4 * (q % nq);
+    const uint32_t off = (static_cast<uint32_t>(m) * a.N + n) * 4;
+    f32x4_t acc = __builtin_bit_cast(
+        f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ws, off, 0, kCachePolicyAgent));
+    int sp = 1;
+    for (; sp + 3 < a.splits; sp += 4) {  // four loads in flight, added in order
+      f32x4_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        v[u] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                               ws, off + (sp + u) * split_bytes, 0, kCachePolicyAgent));
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc += v[u];
+    }
+    for (; sp < a.splits; ++sp)
+      acc += __builtin_bit_cast(
+          f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ws, off + sp * split_bytes, 0, kCachePolicyAgent));
+    const uint32_t lo = static_cast<uint32_t>(float_to_bf16_bits(acc[0])) |
+                        (static_cast<uint32_t>(float_to_bf16_bits(acc[1])) << 16);
+    const uint32_t hi = static_cast<uint32_t>(float_to_bf16_bits(acc[2])) |
+                        (static_cast<uint32_t>(float_to_bf16_bits(acc[3])) << 16);
+    *reinterpret_cast<uint2*>(a.y + static_cast<size_t>(m) * a.N + n) = make_uint2(lo, hi);
   }
-  const uint32_t lo = static_cast<uint32_t>(float_to_bf16_bits(acc.x)) |
-                      (static_cast<uint32_t>(float_to_bf16_bits(acc.y)) << 16);
-  const uint32_t hi = static_cast<uint32_t>(float_to_bf16_bits(acc.z)) |
-                      (static_cast<uint32_t>(float_to_bf16_bits(acc.w)) << 16);
-  reinterpret_cast<uint2*>(y)[i] = make_uint2(lo, hi);
+  if (threadIdx.x == 0) __hip_atomic_store(a.cnt + ng, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Tile ownership shared by both kernels.
@@ -209,20 +241,42 @@ struct TileSet {
 // MFMA kernel.  Workgroup = WAVES wavefronts x NT tiles, all rows, one k-split.  Per
 // chunk of CH blocks, x is copied to LDS (double buffered, one barrier per chunk);
 // each wavefront unpacks its tiles' codes straight into B operands and runs
-// 16x16x32 bf16 MFMAs against A fragments read from LDS.  The per-group sums of x
-// that the zero-point needs come from one more MFMA per A fragment with an all-ones
-// B operand, which lands them in the accumulator layout with no extra VALU work.
+// 16x16x32 bf16 MFMAs against A fragments read from LDS.
+//
+// The zero-point term needs the per-group sums of x.  They are the same for every
+// wavefront, so each row tile has one owner wavefront (row tile mt belongs to
+// wavefront mt % WAVES) that runs one more MFMA per A fragment with an all-ones B
+// operand -- the sums land in the accumulator layout -- and publishes them in LDS.
+// They are visible to the other wavefronts after the chunk's barrier, so the term
+// -c * sum(x) of a chunk is applied at the start of the next one (the offsets c of
+// the chunk are kept in registers until then).
 //
 // LDS layout of a chunk: 16-byte pieces, row-major [row][block][piece], the 16
 // pieces of each (row, block) permuted by piece ^ (row & 7).  Copy-in writes eight
 // consecutive pieces of one row per 8 lanes and an A fragment reads one piece of
 // eight consecutive rows per 8 lanes: both touch eight distinct 16-byte bank groups.
+//
+// All global reads go through buffer resources: 32-bit offsets from a scalar base,
+// and rows past M (offsets past the end of x) read zeros.  Blocks past the split
+// read whatever lies there and are never consumed.
 // ---------------------------------------------------------------------------
 
-template <int ROWS, int CH>
+template <int ROWS, int CH, int GPC>
 struct MfmaLds {
-  static constexpr int PIECES = ROWS * CH * 16;
-  u32x4_t x[2][PIECES];
+  u32x4_t x[2][ROWS * CH * 16];
+  float xs[2][GPC][ROWS];  // per-group sums of x of the chunk in the same buffer
+};
+
+// Global operands of one launch as buffer resources.
+struct QBuffers {
+  __amdgpu_buffer_rsrc_t x, w, s, z;
+  __device__ __forceinline__ QBuffers(const QArgs& a, int bits, int group) {
+    x = buffer_rsrc(a.x, static_cast<uint32_t>(a.M) * a.K * 2);
+    w = buffer_rsrc(a.qw, static_cast<uint32_t>(a.n_tiles) * a.KB * 256 * bits);
+    const uint32_t sz = static_cast<uint32_t>(a.K / group) * a.N * 2;
+    s = buffer_rsrc(a.sc, sz);
+    z = buffer_rsrc(a.zr, sz);
+  }
 };
 
 template <int BITS, int GROUP, int MT, int NT, int CH, int WAVES>
@@ -235,8 +289,12 @@ struct MfmaBody {
   static constexpr int PIECES = ROWS * CH * 16;
   static constexpr int PPT = PIECES / THREADS;  // pieces per thread per chunk
   static_assert(PIECES % THREADS == 0, "a chunk is a whole number of pieces per thread");
-  using Lds = MfmaLds<ROWS, CH>;
-  using W = WChunk<BITS, NT, CH, GPC>;
+  using Lds = MfmaLds<ROWS, CH, GPC>;
+  struct W {
+    Slice<BITS> w[CH][NT];
+    uint32_t s[GPC][NT];  // fp16 bits of the scale
+    uint32_t z[GPC][NT];  // fp16 bits of the zero-point
+  };
   struct X {
     u32x4_t v[PPT];
   };
@@ -245,16 +303,35 @@ struct MfmaBody {
     return row * (CH * 16) + b * 16 + (piece ^ (row & 7));
   }
 
-  // Coalesced copy of chunk (rows x blocks kb..kb+CH-1) into registers; rows past M
-  // and blocks past the split read clamped addresses and are never consumed.
-  static __device__ __forceinline__ void stage_load(X& r, const QArgs& a, int kb, int kb_end) {
+  // Weights of blocks kb..kb+CH-1 for the wavefront's tiles; wofs[t] is the byte
+  // offset of the lane's slice in block 0 of tile t, col[t] its column.
+  static __device__ __forceinline__ void load_w(W& r, const QBuffers& bu, const QArgs& a,
+                                                const uint32_t (&wofs)[NT], const int (&col)[NT],
+                                                int kb) {
+#pragma unroll
+    for (int b = 0; b < CH; ++b)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        r.w[b][t] = load_slice<BITS>(bu.w, wofs[t] + static_cast<uint32_t>(kb + b) * (256 * BITS));
+#pragma unroll
+    for (int gc = 0; gc < GPC; ++gc)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const uint32_t off = (static_cast<uint32_t>(kb * GPB + gc) * a.N + col[t]) * 2;
+        r.s[gc][t] = __builtin_amdgcn_raw_buffer_load_b16(bu.s, off, 0, 0);
+        r.z[gc][t] = __builtin_amdgcn_raw_buffer_load_b16(bu.z, off, 0, 0);
+      }
+  }
+
+  // Coalesced copy of chunk (rows x blocks kb..kb+CH-1) into registers.
+  static __device__ __forceinline__ void stage_load(X& r, const QBuffers& bu, int K, int kb) {
 #pragma unroll
     for (int p = 0; p < PPT; ++p) {
       const int P = p * THREADS + threadIdx.x;
-      const int row = min(P / (CH * 16), a.M - 1), b = (P / 16) % CH, pc = P % 16;
-      const int kbc = min(kb + b, kb_end - 1);
-      r.v[p] = *reinterpret_cast<const u32x4_t*>(a.x + static_cast<size_t>(row) * a.K +
-                                                 static_cast<size_t>(kbc) * kTileK + pc * 8);
+      const int row = P / (CH * 16), b = (P / 16) % CH, pc = P % 16;
+      const uint32_t off =
+          (static_cast<uint32_t>(row) * K + static_cast<uint32_t>(kb + b) * kTileK + pc * 8) * 2;
+      r.v[p] = __builtin_amdgcn_raw_buffer_load_b128(bu.x, off, 0, 0);
     }
   }
 
@@ -267,16 +344,49 @@ struct MfmaBody {
     }
   }
 
-  // Consume one chunk (blocks kb..kb+CH-1 of the split, LDS buffer buf).  Within a
-  // group the k-steps are outermost, so the MT*(NT+1) accumulators of the group form
-  // independent MFMA chains that keep the matrix pipe busy; each is folded into tot
-  // (scale and offset) when the group is complete.
-  static __device__ __forceinline__ void compute(const W& wc, const Lds& lds, int buf, int kb,
-                                                 int kb_end, int lane, f32x4_t (&tot)[MT][NT]) {
+  // The zero-point term of the previous chunk (LDS buffer buf, first block kb):
+  // tot -= c * sum(x) with the offsets c kept from that chunk.
+  static __device__ __forceinline__ void correct(const Lds& L, int buf, int kb, int kb_end, int lane,
+                                                 const float (&cprev)[GPC][NT],
+                                                 f32x4_t (&tot)[MT][NT]) {
+    const int quarter = lane >> 4;
+#pragma unroll
+    for (int b = 0; b < CH; ++b) {
+      if (kb + b < kb_end) {
+#pragma unroll
+        for (int gi = 0; gi < GPB; ++gi) {
+          const int gc = b * GPB + gi;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const f32x4_t xv = *reinterpret_cast<const f32x4_t*>(&L.xs[buf][gc][16 * mt + 4 * quarter]);
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) tot[mt][t][r] = __builtin_fmaf(-cprev[gc][t], xv[r], tot[mt][t][r]);
+          }
+        }
+      }
+    }
+  }
+
+  // Consume one chunk (blocks kb..kb+CH-1 of the split, LDS buffer buf): MFMAs per
+  // group with the k-steps outermost, so the MT*NT accumulators of a group form
+  // independent chains; tot += s * acc when the group is complete.  Every wavefront
+  // also sums x over its duty row tiles wave + WAVES*i (one more A fragment and one
+  // ones-MFMA per step, no branch in the MFMA sequence); owners publish the group's
+  // sums.  cnext receives the chunk's offsets c.
+  static constexpr int DUTY = (MT + WAVES - 1) / WAVES;
+
+  static __device__ __forceinline__ void compute(const W& wc, Lds& L, int buf, int kb, int kb_end,
+                                                 int lane, int wave, f32x4_t (&tot)[MT][NT],
+                                                 float (&cnext)[GPC][NT]) {
     const int col = lane & 15, quarter = lane >> 4;
     const bf16x8_t ones = __builtin_bit_cast(
         bf16x8_t, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    int dmt[DUTY];
+#pragma unroll
+    for (int i = 0; i < DUTY; ++i) dmt[i] = (wave + WAVES * i) % MT;
 #pragma unroll
     for (int b = 0; b < CH; ++b) {
       if (kb + b < kb_end) {
@@ -286,14 +396,14 @@ struct MfmaBody {
 #pragma unroll
         for (int gi = 0; gi < GPB; ++gi) {
           const int gc = b * GPB + gi;
-          f32x4_t acc[MT][NT], accx[MT];
+          f32x4_t acc[MT][NT], accx[DUTY];
 #pragma unroll
           for (int js = 0; js < SPG; ++js) {
             const int j = gi * SPG + js;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
               const bf16x8_t A = __builtin_bit_cast(
-                  bf16x8_t, lds.x[buf][slot(16 * mt + col, b, 4 * j + quarter)]);
+                  bf16x8_t, L.x[buf][slot(16 * mt + col, b, 4 * j + quarter)]);
 #pragma unroll
               for (int t = 0; t < NT; ++t) {
                 const uint4 bw = make_uint4(pr[t][4 * j], pr[t][4 * j + 1], pr[t][4 * j + 2],
@@ -302,22 +412,28 @@ struct MfmaBody {
                 acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                     A, B, js == 0 ? zero : acc[mt][t], 0, 0, 0);
               }
-              accx[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, ones, js == 0 ? zero : accx[mt],
-                                                                 0, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < DUTY; ++i) {
+              const bf16x8_t A = __builtin_bit_cast(
+                  bf16x8_t, L.x[buf][slot(16 * dmt[i] + col, b, 4 * j + quarter)]);
+              accx[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, ones, js == 0 ? zero : accx[i],
+                                                                0, 0, 0);
             }
           }
-          float sv[NT], cv[NT];
+          float sv[NT];
 #pragma unroll
-          for (int t = 0; t < NT; ++t) scale_and_offset(wc.s[gc][t], wc.z[gc][t], sv[t], cv[t]);
+          for (int t = 0; t < NT; ++t) scale_and_offset(wc.s[gc][t], wc.z[gc][t], sv[t], cnext[gc][t]);
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const float v = __builtin_fmaf(sv[t], acc[mt][t][r], tot[mt][t][r]);
-                tot[mt][t][r] = __builtin_fmaf(-cv[t], accx[mt][r], v);
-              }
+              for (int r = 0; r < 4; ++r) tot[mt][t][r] = __builtin_fmaf(sv[t], acc[mt][t][r], tot[mt][t][r]);
+#pragma unroll
+          for (int i = 0; i < DUTY; ++i)
+            if (wave + WAVES * i < MT && col == 0)
+              *reinterpret_cast<f32x4_t*>(&L.xs[buf][gc][16 * dmt[i] + 4 * quarter]) = accx[i];
         }
       }
     }
@@ -328,61 +444,72 @@ template <int BITS, int GROUP, int MT, int NT, int CH, int WAVES, int PF>
 __global__ __launch_bounds__(WAVES * kWave) void k_qgemm_mfma(QArgs a) {
   static_assert(PF % 2 == 0, "the LDS buffer of a chunk follows the ring slot's parity");
   using Body = MfmaBody<BITS, GROUP, MT, NT, CH, WAVES>;
+  constexpr int GPC = Body::GPC;
   __shared__ typename Body::Lds lds;
 
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
   const int ng = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
   const int kb0 = split * a.blocks_per_split;
   const int kb_end = min(a.KB, kb0 + a.blocks_per_split);
   const int nchunks = (kb_end - kb0 + CH - 1) / CH;
-  const TileSet<BITS, NT> ts(a, (ng * WAVES + wave) * NT, lane);
+  const QBuffers bu(a, BITS, GROUP);
+
+  bool ok[NT];
+  int col[NT];
+  uint32_t wofs[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int nt = (ng * WAVES + wave) * NT + t;
+    ok[t] = nt < a.n_tiles;
+    const int ntc = ok[t] ? nt : 0;
+    col[t] = ntc * kTileN + (lane & 15);
+    wofs[t] = static_cast<uint32_t>(ntc) * a.KB * (256 * BITS) + lane * (4 * BITS);
+  }
 
   f32x4_t tot[MT][NT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int t = 0; t < NT; ++t) tot[mt][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float cprev[GPC][NT];
 
-  // Weights: a ring of PF chunks.  Activations: two register sets, so the copy of
-  // chunk c+2 is in flight while chunk c is consumed and chunk c+1 goes to LDS.
+  // Weights and activations: rings of PF chunks each, refilled in the same order
+  // (weights of chunk c+PF, then activations of chunk c+1+PF), so every load is
+  // issued PF chunks before it is waited for.  Loads complete in issue order: an
+  // activation ring shallower than the weight ring would cap the weights' lead too.
   typename Body::W w[PF];
-  typename Body::X x0, x1;
+  typename Body::X x[PF];
   static_for<PF>([&](auto u) __attribute__((always_inline)) {
-    load_wchunk<BITS, GROUP>(w[u.value], a, ts.wbase, ts.ncol, kb0 + u.value * CH, kb_end);
+    Body::load_w(w[u.value], bu, a, wofs, col, kb0 + u.value * CH);
+    Body::stage_load(x[u.value], bu, a.K, kb0 + u.value * CH);
   });
-  Body::stage_load(x0, a, kb0, kb_end);
-  Body::stage_load(x1, a, kb0 + CH, kb_end);
-  Body::stage_store(lds, 0, x0);
+  Body::stage_store(lds, 0, x[0]);
+  Body::stage_load(x[0], bu, a.K, kb0 + PF * CH);
   __syncthreads();
 
-  // One chunk: ring slot U holds chunk c+U; the LDS buffer and the activation register
-  // set follow the chunk's parity (PF is even).  REFILL = false in the drain.
+  // One chunk: ring slot U holds chunk c+U; the LDS buffer follows the chunk's parity
+  // (PF is even).  REFILL = false in the drain.
   auto step = [&](auto u, int c, auto refill) __attribute__((always_inline)) {
     constexpr int U = decltype(u)::value;
+    constexpr int V = (U + 1) % PF;  // slot of chunk c+U+1
     const int kb = kb0 + (c + U) * CH;
-    if constexpr (U % 2 == 0) {
-      Body::stage_load(x0, a, kb + 2 * CH, kb_end);
-    } else {
-      Body::stage_load(x1, a, kb + 2 * CH, kb_end);
-    }
-    Body::compute(w[U], lds, U & 1, kb, kb_end, lane, tot);
-    if constexpr (decltype(refill)::value)
-      load_wchunk<BITS, GROUP>(w[U], a, ts.wbase, ts.ncol, kb + PF * CH, kb_end);
-    if constexpr (U % 2 == 0) {
-      Body::stage_store(lds, 1, x1);
-    } else {
-      Body::stage_store(lds, 0, x0);
-    }
+    if (c + U > 0) Body::correct(lds, (U + 1) & 1, kb - CH, kb_end, lane, cprev, tot);
+    Body::compute(w[U], lds, U & 1, kb, kb_end, lane, wave, tot, cprev);
+    if constexpr (decltype(refill)::value) Body::load_w(w[U], bu, a, wofs, col, kb + PF * CH);
+    Body::stage_store(lds, (U + 1) & 1, x[V]);
+    if constexpr (decltype(refill)::value) Body::stage_load(x[V], bu, a.K, kb + (PF + 1) * CH);
     __syncthreads();
   };
 
-  // Steady state: straight-line body (every load unconditional and clamped) so that
-  // each wait on outstanding loads is exact.  Then drain the last (at most PF)
-  // chunks without further weight loads.
+  // Steady state: straight-line body (every load unconditional) so that each wait on
+  // outstanding loads is exact.  Then drain the last (at most PF) chunks without
+  // further loads, and apply the last chunk's zero-point term.
   int c = 0;
   for (; c + PF < nchunks; c += PF)
     static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::true_type{}); });
   static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::false_type{}); });
+  Body::correct(lds, (PF - 1) & 1, kb0 + (c + PF - 1) * CH, kb_end, lane, cprev, tot);
 
   // D layout of 16x16 MFMA: lane holds column lane%16, rows 4*(lane/16) + r.
   const int quarter = lane >> 4;
@@ -393,8 +520,9 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemm_mfma(QArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = 16 * mt + 4 * quarter + r;
-        if (ts.ok[t] && m < a.M) store_out(a, split, m, ts.ncol[t], tot[mt][t][r]);
+        if (ok[t] && m < a.M) store_out(a, split, m, col[t], tot[mt][t][r]);
       }
+  if (a.splits > 1) finish_splitk<WAVES * kWave>(a, ng, WAVES * NT * kTileN);
 }
 
 // ---------------------------------------------------------------------------
@@ -566,6 +694,7 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t)
       if (ts.ok[t] && (m & 3) == quarter && m < a.M) store_out(a, split, m, ts.ncol[t], tot[m][t]);
+  if (a.splits > 1) finish_splitk<THREADS>(a, ng, WAVES * NT * kTileN);
 }
 
 // ---------------------------------------------------------------------------
@@ -624,12 +753,6 @@ hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QAr
   if (!v) return hipErrorInvalidDeviceFunction;
   const size_t lds = kc.path == 1 ? gemv_lds_bytes(kc.rows, a.blocks_per_split * kTileK, group) : 0;
   hipLaunchKernelGGL(v->fn, dim3(grid), dim3(kc.waves * kWave), lds, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.splits == 1) return e;
-  const size_t quads = static_cast<size_t>(a.M) * a.N / 4;
-  const unsigned rgrid = static_cast<unsigned>((quads + kThreadsPerBlock - 1) / kThreadsPerBlock);
-  hipLaunchKernelGGL(k_splitk_reduce, dim3(rgrid), dim3(kThreadsPerBlock), 0, st, a.ws, a.y, a.M,
-                     a.N, a.splits);
   return hipGetLastError();
 }
 

@@ -83,6 +83,8 @@ def test_host_packer_round_trip_exhaustive(bits):
     (9, 512, 256, 4, 64, 1, "EUNSUPPORTED"),
     (4, 512, 256, 4, 64, 7, "EINVAL"),
     (4, -16, 256, 4, 64, 0, "EINVAL"),
+    (4, 1 << 20, 1 << 13, 4, 64, 0, "EUNSUPPORTED"),   # N*K > 2^32
+    (4, 16, (1 << 24) + 128, 4, 64, 0, "EUNSUPPORTED"),  # K > 2^24
 ])
 def test_plan_rejects_bad_shapes(M, N, K, bits, group, path, err):
     with pytest.raises(ss.SubspecError) as ei:
@@ -105,7 +107,8 @@ def test_plan_choices_are_consistent():
                 if p["splits"] == 1:
                     assert p["workspace_bytes"] == 0
                 else:
-                    assert p["workspace_bytes"] == p["splits"] * M * N * 4
+                    # completion counters (16384 x 4 bytes), then the fp32 partial sums
+                    assert p["workspace_bytes"] == 65536 + p["splits"] * M * N * 4
     assert ss.subspec_qlinear_plan(2, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_GEMV
     assert ss.subspec_qlinear_plan(3, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_MFMA
     assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_GEMV)["path"] == ss.SUBSPEC_PATH_GEMV
