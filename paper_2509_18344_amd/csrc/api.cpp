@@ -65,6 +65,8 @@ struct Tuning {
   int gemv_max_m = kAutoGemvMaxRows;  // largest M the automatic plan sends to the GEMV path
   int target_blocks = 0;          // workgroups to aim for; 0 = one full residency round
   int gemv_nt = 1;
+  int gemv_waves = 4;
+  int gemv_ch = 4;
   int mfma_nt = 0;                // tiles per MFMA wavefront; 0 = choose per shape
   int splits = 0;                 // 0 = choose per shape
   int partial_div = 2;            // split-K partial traffic may reach weight bytes / this
@@ -89,6 +91,8 @@ const Tuning& tuning() {
         if (k == "gemv_max_m") r.gemv_max_m = v;
         else if (k == "target") r.target_blocks = v;
         else if (k == "gemv_nt") r.gemv_nt = v;
+        else if (k == "gemv_waves") r.gemv_waves = v;
+        else if (k == "gemv_ch") r.gemv_ch = v;
         else if (k == "mfma_nt") r.mfma_nt = v;
         else if (k == "splits") r.splits = v;
         else if (k == "partial_div") r.partial_div = v;
@@ -133,39 +137,63 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c.path = 1;
     c.rows = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 8;
     c.nt = tu.gemv_nt;
-    c.chunk = 4;
+    c.waves = tu.gemv_waves;
+    c.chunk = tu.gemv_ch;
   } else if (path == SUBSPEC_PATH_MFMA) {
     c.path = 2;
     const int mt = M <= 16 ? 1 : M <= 32 ? 2 : M <= 64 ? 4 : 8;
     c.rows = 16 * mt;
     // LDS holds two chunks of rows x (128*chunk) activations: ~34 KB up to M = 64.
     c.chunk = mt == 1 ? 4 : mt == 2 ? 2 : 1;
-    // From 64 rows on, two tiles per wavefront halve the activation reads from LDS
-    // (the A fragments are shared by the wavefront's tiles).
-    c.nt = tu.mfma_nt ? tu.mfma_nt : (mt >= 4 ? 2 : 1);
+    c.nt = tu.mfma_nt ? tu.mfma_nt : 1;
   } else {
     return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
   }
   if (!subspec::qlinear_variant_exists(c, bits, group))
     return fail(SUBSPEC_EUNSUPPORTED, "no kernel for path=%d rows=%d nt=%d chunk=%d waves=%d bits=%d group=%d",
                 c.path, c.rows, c.nt, c.chunk, c.waves, bits, group);
+
+  // Workgroups that fit on the device at once (one residency round).
+  auto resident_of = [&](const subspec::KernelChoice& k) {
+    if (tu.target_blocks > 0) return tu.target_blocks;
+    size_t lds = 0;
+    if (k.path == 1) {
+      const int cols = k.waves * k.nt * subspec::kTileN;
+      lds = subspec::gemv_lds_bytes(k.rows, std::min(K, subspec::gemv_max_kspan(k.rows, k.waves, group, cols)),
+                                    group, cols);
+    }
+    int per_cu = subspec::qlinear_resident_blocks(k, bits, group, lds);
+    if (per_cu <= 0) per_cu = 2;
+    return per_cu * device_cus();
+  };
+  auto groups_of = [&](const subspec::KernelChoice& k) {
+    const int cols = k.waves * k.nt * subspec::kTileN;
+    return (N + cols - 1) / cols;
+  };
+  int resident = resident_of(c);
+  // A launch with more column groups than fit at once would run in several rounds;
+  // two tiles per wavefront (half the workgroups, and each A fragment read from LDS
+  // feeds two MFMAs) keep it to one when that variant fits.
+  if (c.path == 2 && !tu.mfma_nt && groups_of(c) > resident) {
+    subspec::KernelChoice c2 = c;
+    c2.nt = 2;
+    if (subspec::qlinear_variant_exists(c2, bits, group)) {
+      const int r2 = resident_of(c2);
+      const long long rounds1 = (groups_of(c) + resident - 1) / resident;
+      const long long rounds2 = (groups_of(c2) + r2 - 1) / r2;
+      if (rounds2 < rounds1) {
+        c = c2;
+        resident = r2;
+      }
+    }
+  }
   const int cols_per_group = c.waves * c.nt * subspec::kTileN;
-  const int col_groups = (N + cols_per_group - 1) / cols_per_group;
+  const int col_groups = groups_of(c);
   const int chunks = (KB + c.chunk - 1) / c.chunk;
 
   // Split K across workgroups only as far as one residency round reaches, and only
   // while the fp32 partial sums (written once, read once) stay a modest fraction of
   // the weight bytes.
-  int resident = 0;
-  if (tu.target_blocks > 0) {
-    resident = tu.target_blocks;
-  } else {
-    size_t lds = 0;
-    if (c.path == 1) lds = subspec::gemv_lds_bytes(c.rows, std::min(K, subspec::gemv_max_kspan(c.rows, c.waves)), group);
-    int per_cu = subspec::qlinear_resident_blocks(c, bits, group, lds);
-    if (per_cu <= 0) per_cu = 2;
-    resident = per_cu * device_cus();
-  }
   int splits = std::max(1, resident / col_groups);
   const double wbytes = static_cast<double>(N) * K * bits / 8 + 4.0 * N * (K / group);
   const double per_split = 8.0 * M * N;
@@ -174,7 +202,8 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   if (tu.splits > 0) splits = tu.splits;
   if (c.path == 1) {
     // the split's activations must fit the GEMV kernel's LDS staging
-    const int max_chunks = subspec::gemv_max_kspan(c.rows, c.waves) / subspec::kTileK / c.chunk;
+    const int max_chunks = std::max(1, subspec::gemv_max_kspan(c.rows, c.waves, group, cols_per_group) /
+                                           subspec::kTileK / c.chunk);
     const int min_splits = (chunks + max_chunks - 1) / max_chunks;
     if (splits < min_splits) splits = min_splits;
   }

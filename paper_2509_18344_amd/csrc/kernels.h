@@ -41,10 +41,11 @@ hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QAr
 bool qlinear_variant_exists(const KernelChoice& kc, int bits, int group);
 // Workgroups of this variant that fit on one compute unit (0 if unknown, e.g. no GPU).
 int qlinear_resident_blocks(const KernelChoice& kc, int bits, int group, size_t dyn_lds);
-// GEMV path: the whole split's activations live in LDS, so a split may span at most
-// gemv_max_kspan(rows) inputs; gemv_lds_bytes is the dynamic LDS of one workgroup.
-int gemv_max_kspan(int rows, int waves);
-size_t gemv_lds_bytes(int rows, int kspan, int group);
+// GEMV path: the whole split's activations and the scales/offsets of its groups live
+// in LDS, so a split may span at most gemv_max_kspan inputs; gemv_lds_bytes is the
+// dynamic LDS of one workgroup (cols = columns of the workgroup).
+int gemv_max_kspan(int rows, int waves, int group, int cols);
+size_t gemv_lds_bytes(int rows, int kspan, int group, int cols);
 
 hipError_t launch_quantize(const float* w, int bits, int group, int N, int K, uint8_t* codes,
                            uint16_t* sc, uint16_t* zr, hipStream_t st);

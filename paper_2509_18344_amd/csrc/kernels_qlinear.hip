@@ -534,27 +534,56 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemm_mfma(QArgs a) {
 // ---------------------------------------------------------------------------
 
 constexpr int kGemvSpans = 2;  // 32-k activation spans staged per thread
+constexpr size_t kGemvLdsBudget = 48 * 1024;  // dynamic LDS per workgroup (3 fit a CU)
+constexpr int kGemvSzRounds = 2;  // (group, 8-column) scale pieces staged per thread
 
-// Dynamic LDS layout: x [ROWS][kspan + 8] bf16, then xsum [kspan/GROUP][ROWS][4] f32.
+// Dynamic LDS layout: x [ROWS][kspan + 8] bf16, xsum [kspan/GROUP][ROWS][4] f32, then
+// sc [kspan/GROUP][cols] (s, c = s * (128 + z)) f32 pairs for the workgroup's columns.
 __host__ __device__ constexpr int gemv_x_stride(int kspan) { return kspan + 8; }
 __host__ __device__ constexpr size_t gemv_xsum_offset(int rows, int kspan) {
   return (static_cast<size_t>(rows) * gemv_x_stride(kspan) * 2 + 15) / 16 * 16;
 }
-size_t gemv_lds_bytes(int rows, int kspan, int group) {
+__host__ __device__ constexpr size_t gemv_sc_offset(int rows, int kspan, int group) {
   return gemv_xsum_offset(rows, kspan) + static_cast<size_t>(kspan / group) * rows * 4 * 4;
 }
-int gemv_max_kspan(int rows, int waves) { return waves * kWave * kGemvSpans * 32 / rows; }
+size_t gemv_lds_bytes(int rows, int kspan, int group, int cols) {
+  return gemv_sc_offset(rows, kspan, group) + static_cast<size_t>(kspan / group) * cols * 8;
+}
+int gemv_max_kspan(int rows, int waves, int group, int cols) {
+  const int staged = waves * kWave * kGemvSpans * 32 / rows;  // what the prologue copies
+  const size_t per_block = gemv_lds_bytes(rows, kTileK, group, cols) - 16;  // bytes per 128 k
+  const int fit = static_cast<int>((kGemvLdsBudget - 16) / per_block) * kTileK;
+  const int sz_groups = kGemvSzRounds * waves * kWave / (cols / 8);  // scale pieces staged
+  const int sz_fit = sz_groups / (kTileK / group) * kTileK;
+  return min(min(staged, sz_fit), max(fit, kTileK));
+}
+
+template <int BITS, int NT, int CH>
+struct GemvW {
+  Slice<BITS> w[CH][NT];
+};
 
 template <int BITS, int GROUP, int ROWS, int NT, int CH>
 struct GemvBody {
   static constexpr int GPB = kTileK / GROUP;
   static constexpr int SPG = 4 / GPB;
-  static constexpr int GPC = CH * GPB;
-  using W = WChunk<BITS, NT, CH, GPC>;
+  using W = GemvW<BITS, NT, CH>;
+
+  // Weights of local blocks kb..kb+CH-1 (buffer loads; blocks past the split read
+  // the next data and are never consumed).
+  static __device__ __forceinline__ void load(W& r, __amdgpu_buffer_rsrc_t wr,
+                                              const uint32_t (&wofs)[NT], int kb) {
+#pragma unroll
+    for (int b = 0; b < CH; ++b)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        r.w[b][t] = load_slice<BITS>(wr, wofs[t] + static_cast<uint32_t>(kb + b) * (256 * BITS));
+  }
 
   // Consume one chunk: local blocks lb..lb+CH-1 of the split (nblk valid).
   static __device__ __forceinline__ void compute(const W& wc, const uint16_t* xl, const float* xsum,
-                                                 int xs, int lb, int nblk, int quarter,
+                                                 const float2* sc, int xs, int cols, int lb,
+                                                 int nblk, int quarter, const int (&lcol)[NT],
                                                  float (&tot)[ROWS][NT]) {
 #pragma unroll
     for (int b = 0; b < CH; ++b) {
@@ -564,12 +593,11 @@ struct GemvBody {
         for (int t = 0; t < NT; ++t) unpack_pairs<BITS>(wc.w[b][t], pr[t]);
 #pragma unroll
         for (int gi = 0; gi < GPB; ++gi) {
-          const int gc = b * GPB + gi;
-          float acc[ROWS][NT];
+          float acc[ROWS][NT], acc2[ROWS][NT];
 #pragma unroll
           for (int m = 0; m < ROWS; ++m)
 #pragma unroll
-            for (int t = 0; t < NT; ++t) acc[m][t] = 0.f;
+            for (int t = 0; t < NT; ++t) acc[m][t] = acc2[m][t] = 0.f;
 #pragma unroll
           for (int js = 0; js < SPG; ++js) {
             const int j = gi * SPG + js;
@@ -579,26 +607,28 @@ struct GemvBody {
                   xl + m * xs + (lb + b) * kTileK + 32 * j + 8 * quarter, 16));
 #pragma unroll
               for (int t = 0; t < NT; ++t) {
-                float v = acc[m][t];
-                v = dot2_bf16(xv.x, pr[t][4 * j + 0], v);
-                v = dot2_bf16(xv.y, pr[t][4 * j + 1], v);
-                v = dot2_bf16(xv.z, pr[t][4 * j + 2], v);
-                v = dot2_bf16(xv.w, pr[t][4 * j + 3], v);
-                acc[m][t] = v;
+                // two chains per (row, tile) halve the dependent dot-product latency
+                float v0 = acc[m][t], v1 = acc2[m][t];
+                v0 = dot2_bf16(xv.x, pr[t][4 * j + 0], v0);
+                v1 = dot2_bf16(xv.y, pr[t][4 * j + 1], v1);
+                v0 = dot2_bf16(xv.z, pr[t][4 * j + 2], v0);
+                v1 = dot2_bf16(xv.w, pr[t][4 * j + 3], v1);
+                acc[m][t] = v0;
+                acc2[m][t] = v1;
               }
             }
           }
-          float sv[NT], cv[NT];
-#pragma unroll
-          for (int t = 0; t < NT; ++t) scale_and_offset(wc.s[gc][t], wc.z[gc][t], sv[t], cv[t]);
           const int g = (lb + b) * GPB + gi;  // group index within the split
+          float2 scv[NT];
+#pragma unroll
+          for (int t = 0; t < NT; ++t) scv[t] = sc[g * cols + lcol[t]];
 #pragma unroll
           for (int m = 0; m < ROWS; ++m) {
             const float xq = xsum[(g * ROWS + m) * 4 + quarter];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-              const float v = __builtin_fmaf(sv[t], acc[m][t], tot[m][t]);
-              tot[m][t] = __builtin_fmaf(-cv[t], xq, v);
+              const float v = __builtin_fmaf(scv[t].x, acc[m][t] + acc2[m][t], tot[m][t]);
+              tot[m][t] = __builtin_fmaf(-scv[t].y, xq, v);
             }
           }
         }
@@ -610,6 +640,8 @@ struct GemvBody {
 template <int BITS, int GROUP, int ROWS, int NT, int CH, int WAVES, int PF>
 __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
   constexpr int THREADS = WAVES * kWave;
+  constexpr int COLS = WAVES * NT * kTileN;
+  constexpr int GPB = kTileK / GROUP;
   using Body = GemvBody<BITS, GROUP, ROWS, NT, CH>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
@@ -624,14 +656,25 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
   const int xs = gemv_x_stride(kspan);
   uint16_t* xl = reinterpret_cast<uint16_t*>(smem);
   float* xsum = reinterpret_cast<float*>(smem + gemv_xsum_offset(ROWS, kspan));
-  const TileSet<BITS, NT> ts(a, (ng * WAVES + wave) * NT, lane);
+  float2* sc = reinterpret_cast<float2*>(smem + gemv_sc_offset(ROWS, kspan, GROUP));
+  const QBuffers bu(a, BITS, GROUP);
+  const int n0 = ng * COLS;
 
-  // Start the weight stream before staging the activations.
+  bool ok[NT];
+  int col[NT], lcol[NT];
+  uint32_t wofs[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int nt = (ng * WAVES + wave) * NT + t;
+    ok[t] = nt < a.n_tiles;
+    const int ntc = ok[t] ? nt : 0;
+    col[t] = ntc * kTileN + (lane & 15);
+    lcol[t] = (wave * NT + t) * kTileN + (lane & 15);
+    wofs[t] = (static_cast<uint32_t>(ntc) * a.KB + kb0) * (256 * BITS) + lane * (4 * BITS);
+  }
+
   typename Body::W w[PF];
-  static_for<PF>([&](auto u) __attribute__((always_inline)) {
-    load_wchunk<BITS, GROUP>(w[u.value], a, ts.wbase, ts.ncol, kb0 + u.value * CH, kb_end);
-  });
-
+  u32x4_t szs[kGemvSzRounds], szz[kGemvSzRounds];
   // Stage x[0..ROWS)[split] (rows past M repeat row M-1 and are never stored) and the
   // per-quarter group sums: piece q of a span is the quarter-q slice of its 32 k.
   {
@@ -640,6 +683,22 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
     const int total = ROWS * spans_per_row;
     SpanRegs<kGemvSpans> r;
     load_spans<kGemvSpans, THREADS>(r, a, kb0, kb_end, spans_per_row, total);
+    // Scales and zero-points of the split's groups for the workgroup's columns: one
+    // (group, 8 columns) piece of s and of z per thread and round, 16-byte loads.
+    const int ngroups = nblk * GPB;
+#pragma unroll
+    for (int p = 0; p < kGemvSzRounds; ++p) {
+      const int q = min(p * THREADS + static_cast<int>(threadIdx.x), ngroups * (COLS / 8) - 1);
+      const int g = q / (COLS / 8), c8 = q % (COLS / 8);
+      const uint32_t off = (static_cast<uint32_t>(kb0 * GPB + g) * a.N + n0 + 8 * c8) * 2;
+      szs[p] = __builtin_amdgcn_raw_buffer_load_b128(bu.s, off, 0, 0);
+      szz[p] = __builtin_amdgcn_raw_buffer_load_b128(bu.z, off, 0, 0);
+    }
+    // The weight stream starts right after these (small) loads: loads complete in
+    // issue order, so the staging is not held up behind it.
+    static_for<PF>([&](auto u) __attribute__((always_inline)) {
+      Body::load(w[u.value], bu.w, wofs, u.value * CH);
+    });
 #pragma unroll
     for (int p = 0; p < kGemvSpans; ++p) {
       const int i = p * THREADS + threadIdx.x;
@@ -656,6 +715,23 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
               make_float4(qs[0], qs[1], qs[2], qs[3]);
       }
     }
+    // Scales and offsets (s, c = s * (128 + z)) of the loaded pieces.
+#pragma unroll
+    for (int p = 0; p < kGemvSzRounds; ++p) {
+      const int q = p * THREADS + threadIdx.x;
+      if (q < ngroups * (COLS / 8)) {
+        const int g = q / (COLS / 8), c8 = q % (COLS / 8);
+        float4* dst = reinterpret_cast<float4*>(sc + g * COLS + 8 * c8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float s0 = half_bits_to_float(static_cast<uint16_t>(szs[p][e]));
+          const float s1 = half_bits_to_float(static_cast<uint16_t>(szs[p][e] >> 16));
+          const float z0 = half_bits_to_float(static_cast<uint16_t>(szz[p][e]));
+          const float z1 = half_bits_to_float(static_cast<uint16_t>(szz[p][e] >> 16));
+          dst[e] = make_float4(s0, s0 * (kCodeBias + z0), s1, s1 * (kCodeBias + z1));
+        }
+      }
+    }
   }
   __syncthreads();
 
@@ -665,17 +741,18 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) tot[m][t] = 0.f;
 
-  // Steady state with unconditional (clamped) refills, then a load-free drain.
+  // Steady state with unconditional refills, then a load-free drain.
   int c = 0;
   for (; c + PF < nchunks; c += PF) {
     static_for<PF>([&](auto u) __attribute__((always_inline)) {
       constexpr int U = decltype(u)::value;
-      Body::compute(w[U], xl, xsum, xs, (c + U) * CH, nblk, quarter, tot);
-      load_wchunk<BITS, GROUP>(w[U], a, ts.wbase, ts.ncol, kb0 + (c + U + PF) * CH, kb_end);
+      Body::compute(w[U], xl, xsum, sc, xs, COLS, (c + U) * CH, nblk, quarter, lcol, tot);
+      Body::load(w[U], bu.w, wofs, (c + U + PF) * CH);
     });
   }
   static_for<PF>([&](auto u) __attribute__((always_inline)) {
-    Body::compute(w[decltype(u)::value], xl, xsum, xs, (c + decltype(u)::value) * CH, nblk, quarter, tot);
+    Body::compute(w[decltype(u)::value], xl, xsum, sc, xs, COLS, (c + decltype(u)::value) * CH, nblk,
+                  quarter, lcol, tot);
   });
 
   // Split-K inside the wavefront: the four quarters hold partial sums of the same
@@ -693,8 +770,8 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
   for (int m = 0; m < ROWS; ++m)
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-      if (ts.ok[t] && (m & 3) == quarter && m < a.M) store_out(a, split, m, ts.ncol[t], tot[m][t]);
-  if (a.splits > 1) finish_splitk<THREADS>(a, ng, WAVES * NT * kTileN);
+      if (ok[t] && (m & 3) == quarter && m < a.M) store_out(a, split, m, col[t], tot[m][t]);
+  if (a.splits > 1) finish_splitk<THREADS>(a, ng, COLS);
 }
 
 // ---------------------------------------------------------------------------
@@ -714,10 +791,13 @@ struct Variant {
 #define SUBSPEC_BG(X) X(4, 128) X(4, 64) X(3, 128) X(3, 64) X(2, 128) X(2, 64)
 #define SUBSPEC_GEMV_SET(B, G)                                                                \
   SUBSPEC_GEMV(B, G, 1, 1, 4, 4, 4), SUBSPEC_GEMV(B, G, 2, 1, 4, 4, 4),                       \
-      SUBSPEC_GEMV(B, G, 4, 1, 4, 4, 2), SUBSPEC_GEMV(B, G, 8, 1, 4, 4, 2),
+      SUBSPEC_GEMV(B, G, 4, 1, 4, 4, 2), SUBSPEC_GEMV(B, G, 8, 1, 4, 4, 2),                   \
+      SUBSPEC_GEMV(B, G, 1, 1, 4, 2, 4), SUBSPEC_GEMV(B, G, 2, 1, 4, 2, 4),                   \
+      SUBSPEC_GEMV(B, G, 1, 1, 4, 8, 4), SUBSPEC_GEMV(B, G, 1, 1, 2, 4, 8),                   \
+      SUBSPEC_GEMV(B, G, 1, 1, 1, 4, 16),
 #define SUBSPEC_MFMA_SET(B, G)                                                                \
   SUBSPEC_MFMA(B, G, 1, 1, 4, 4, 2), SUBSPEC_MFMA(B, G, 2, 1, 2, 4, 2),                       \
-      SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 4), SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2),                   \
+      SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2),                   \
       SUBSPEC_MFMA(B, G, 1, 2, 4, 4, 2), SUBSPEC_MFMA(B, G, 2, 2, 2, 4, 2),                   \
       SUBSPEC_MFMA(B, G, 4, 2, 1, 4, 4), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),
 
@@ -751,7 +831,9 @@ hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QAr
                           hipStream_t st) {
   const Variant* v = find_variant(kc, bits, group);
   if (!v) return hipErrorInvalidDeviceFunction;
-  const size_t lds = kc.path == 1 ? gemv_lds_bytes(kc.rows, a.blocks_per_split * kTileK, group) : 0;
+  const size_t lds = kc.path == 1 ? gemv_lds_bytes(kc.rows, a.blocks_per_split * kTileK, group,
+                                                   kc.waves * kc.nt * kTileN)
+                                  : 0;
   hipLaunchKernelGGL(v->fn, dim3(grid), dim3(kc.waves * kWave), lds, st, a);
   return hipGetLastError();
 }
