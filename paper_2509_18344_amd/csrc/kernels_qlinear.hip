@@ -694,11 +694,10 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
       szs[p] = __builtin_amdgcn_raw_buffer_load_b128(bu.s, off, 0, 0);
       szz[p] = __builtin_amdgcn_raw_buffer_load_b128(bu.z, off, 0, 0);
     }
-    // The weight stream starts right after these (small) loads: loads complete in
-    // issue order, so the staging is not held up behind it.
-    static_for<PF>([&](auto u) __attribute__((always_inline)) {
-      Body::load(w[u.value], bu.w, wofs, u.value * CH);
-    });
+    // The weight stream starts right after these (small) loads with one chunk: loads
+    // complete in issue order, and a smaller first burst lets the activations (which
+    // every wavefront needs before it can start) return sooner.
+    Body::load(w[0], bu.w, wofs, 0);
 #pragma unroll
     for (int p = 0; p < kGemvSpans; ++p) {
       const int i = p * THREADS + threadIdx.x;
@@ -734,6 +733,10 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
     }
   }
   __syncthreads();
+
+  static_for<PF - 1>([&](auto u) __attribute__((always_inline)) {
+    Body::load(w[u.value + 1], bu.w, wofs, (u.value + 1) * CH);
+  });
 
   float tot[ROWS][NT];
 #pragma unroll
