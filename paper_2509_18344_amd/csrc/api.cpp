@@ -66,8 +66,12 @@ struct Tuning {
   int target_blocks = 0;          // workgroups to aim for; 0 = one full residency round
   int gemv_nt = 1;
   int gemv_waves = 4;
-  int gemv_ch = 4;
+  int gemv_ch = 0;                // 128-k blocks per GEMV ring stage; 0 = choose per M
+  int gemv_pf = 0;                // ring depth in stages; 0 = the variant's
   int mfma_nt = 0;                // tiles per MFMA wavefront; 0 = choose per shape
+  int mfma_ch = 0;
+  int mfma_pf = 0;
+  int wg_per_cu = 0;              // split-K target workgroups per CU; 0 = path default
   int splits = 0;                 // 0 = choose per shape
   int partial_div = 2;            // split-K partial traffic may reach weight bytes / this
 };
@@ -93,7 +97,11 @@ const Tuning& tuning() {
         else if (k == "gemv_nt") r.gemv_nt = v;
         else if (k == "gemv_waves") r.gemv_waves = v;
         else if (k == "gemv_ch") r.gemv_ch = v;
+        else if (k == "gemv_pf") r.gemv_pf = v;
         else if (k == "mfma_nt") r.mfma_nt = v;
+        else if (k == "mfma_ch") r.mfma_ch = v;
+        else if (k == "mfma_pf") r.mfma_pf = v;
+        else if (k == "wg_per_cu") r.wg_per_cu = v;
         else if (k == "splits") r.splits = v;
         else if (k == "partial_div") r.partial_div = v;
       }
@@ -138,13 +146,19 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c.rows = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 8;
     c.nt = tu.gemv_nt;
     c.waves = tu.gemv_waves;
-    c.chunk = tu.gemv_ch;
+    // A shallow ring (two stages of two blocks for one or two rows) keeps register
+    // use low enough for more resident waves; measured faster than deeper rings.
+    c.chunk = tu.gemv_ch ? tu.gemv_ch : c.rows <= 2 ? 2 : 4;
+    c.prefetch = tu.gemv_pf;
   } else if (path == SUBSPEC_PATH_MFMA) {
     c.path = 2;
     const int mt = M <= 16 ? 1 : M <= 32 ? 2 : M <= 64 ? 4 : 8;
     c.rows = 16 * mt;
-    // LDS holds two chunks of rows x (128*chunk) activations: ~34 KB up to M = 64.
-    c.chunk = mt == 1 ? 4 : mt == 2 ? 2 : 1;
+    // LDS holds two chunks of rows x (128*chunk) activations (at most 64 KB).  Short
+    // ring stages (256 k for one row tile, 128 k beyond) keep register use low enough
+    // for a third resident workgroup; measured faster than longer stages.
+    c.chunk = tu.mfma_ch ? tu.mfma_ch : mt == 1 ? 2 : 1;
+    c.prefetch = tu.mfma_pf;
     c.nt = tu.mfma_nt ? tu.mfma_nt : 1;
   } else {
     return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
@@ -191,10 +205,16 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   const int col_groups = groups_of(c);
   const int chunks = (KB + c.chunk - 1) / c.chunk;
 
-  // Split K across workgroups only as far as one residency round reaches, and only
-  // while the fp32 partial sums (written once, read once) stay a modest fraction of
-  // the weight bytes.
-  int splits = std::max(1, resident / col_groups);
+  // Split K across workgroups only as far as a target workgroup count reaches, and
+  // only while the fp32 partial sums (written once, read once) stay a modest fraction
+  // of the weight bytes.  The target is two workgroups per CU (or one residency
+  // round, if smaller): their waves already keep enough loads in flight, and further
+  // splits only add partial traffic (measured on the 7B MLP with both paths: 592
+  // column groups run faster unsplit than split in two, 56 faster in 9 splits than
+  // in 13).
+  const int per_cu_target = tu.wg_per_cu ? tu.wg_per_cu : 2;
+  const int target = tu.target_blocks ? resident : std::min(resident, per_cu_target * device_cus());
+  int splits = std::max(1, target / col_groups);
   const double wbytes = static_cast<double>(N) * K * bits / 8 + 4.0 * N * (K / group);
   const double per_split = 8.0 * M * N;
   const int cap = std::max(1, static_cast<int>(wbytes / (tu.partial_div * per_split)));

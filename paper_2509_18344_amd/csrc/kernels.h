@@ -34,6 +34,7 @@ struct KernelChoice {
   int nt;      // tiles per wavefront
   int chunk;   // 128-k blocks per LDS stage
   int waves;   // wavefronts per workgroup (4 or 8)
+  int prefetch = 0;  // ring depth in chunks; 0 = the variant table's choice
 };
 
 hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a,

@@ -793,23 +793,21 @@ struct Variant {
   {2, 16 * MT, T, C, W, P, B, G, k_qgemm_mfma<B, G, MT, T, C, W, P>}
 #define SUBSPEC_BG(X) X(4, 128) X(4, 64) X(3, 128) X(3, 64) X(2, 128) X(2, 64)
 #define SUBSPEC_GEMV_SET(B, G)                                                                \
-  SUBSPEC_GEMV(B, G, 1, 1, 4, 4, 4), SUBSPEC_GEMV(B, G, 2, 1, 4, 4, 4),                       \
-      SUBSPEC_GEMV(B, G, 4, 1, 4, 4, 2), SUBSPEC_GEMV(B, G, 8, 1, 4, 4, 2),                   \
-      SUBSPEC_GEMV(B, G, 1, 1, 4, 2, 4), SUBSPEC_GEMV(B, G, 2, 1, 4, 2, 4),                   \
-      SUBSPEC_GEMV(B, G, 1, 1, 4, 8, 4), SUBSPEC_GEMV(B, G, 1, 1, 2, 4, 8),                   \
-      SUBSPEC_GEMV(B, G, 1, 1, 1, 4, 16),
+  SUBSPEC_GEMV(B, G, 1, 1, 2, 4, 2), SUBSPEC_GEMV(B, G, 2, 1, 2, 4, 2),                       \
+      SUBSPEC_GEMV(B, G, 4, 1, 4, 4, 2), SUBSPEC_GEMV(B, G, 8, 1, 4, 4, 2),
 #define SUBSPEC_MFMA_SET(B, G)                                                                \
-  SUBSPEC_MFMA(B, G, 1, 1, 4, 4, 2), SUBSPEC_MFMA(B, G, 2, 1, 2, 4, 2),                       \
-      SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2),                   \
-      SUBSPEC_MFMA(B, G, 1, 2, 4, 4, 2), SUBSPEC_MFMA(B, G, 2, 2, 2, 4, 2),                   \
-      SUBSPEC_MFMA(B, G, 4, 2, 1, 4, 4), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),
+  SUBSPEC_MFMA(B, G, 1, 1, 2, 4, 2), SUBSPEC_MFMA(B, G, 1, 2, 2, 4, 2),                       \
+      SUBSPEC_MFMA(B, G, 2, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 2, 2, 1, 4, 2),                   \
+      SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 4, 2, 1, 4, 4),                   \
+      SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),
 
 static const Variant kVariants[] = {SUBSPEC_BG(SUBSPEC_GEMV_SET) SUBSPEC_BG(SUBSPEC_MFMA_SET)};
 
 static const Variant* find_variant(const KernelChoice& kc, int bits, int group) {
   for (const Variant& v : kVariants)
     if (v.path == kc.path && v.rows == kc.rows && v.nt == kc.nt && v.chunk == kc.chunk &&
-        v.waves == kc.waves && v.bits == bits && v.group == group)
+        v.waves == kc.waves && v.bits == bits && v.group == group &&
+        (kc.prefetch == 0 || v.prefetch == kc.prefetch))
       return &v;
   return nullptr;
 }
