@@ -265,6 +265,7 @@ template <int ROWS, int CH, int GPC>
 struct MfmaLds {
   u32x4_t x[2][ROWS * CH * 16];
   float xs[2][GPC][ROWS];  // per-group sums of x of the chunk in the same buffer
+  f32x4_t sink[kWave];     // target of the lanes that do not publish sums
 };
 
 // Global operands of one launch as buffer resources.
@@ -346,13 +347,14 @@ struct MfmaBody {
 
   // The zero-point term of the previous chunk (LDS buffer buf, first block kb):
   // tot -= c * sum(x) with the offsets c kept from that chunk.
+  template <bool FULL>
   static __device__ __forceinline__ void correct(const Lds& L, int buf, int kb, int kb_end, int lane,
                                                  const float (&cprev)[GPC][NT],
                                                  f32x4_t (&tot)[MT][NT]) {
     const int quarter = lane >> 4;
 #pragma unroll
     for (int b = 0; b < CH; ++b) {
-      if (kb + b < kb_end) {
+      if (FULL || kb + b < kb_end) {
 #pragma unroll
         for (int gi = 0; gi < GPB; ++gi) {
           const int gc = b * GPB + gi;
@@ -371,37 +373,34 @@ struct MfmaBody {
 
   // Consume one chunk (blocks kb..kb+CH-1 of the split, LDS buffer buf): MFMAs per
   // group with the k-steps outermost, so the MT*NT accumulators of a group form
-  // independent chains; tot += s * acc when the group is complete.  Every wavefront
-  // also sums x over its duty row tiles wave + WAVES*i (one more A fragment and one
-  // ones-MFMA per step, no branch in the MFMA sequence); owners publish the group's
-  // sums.  cnext receives the chunk's offsets c.
-  static constexpr int DUTY = (MT + WAVES - 1) / WAVES;
-
+  // independent chains; tot += s * acc when the group is complete.  The wavefront
+  // with index DW also sums x over its row tiles DW, DW+WAVES, ... (one ones-MFMA
+  // per A fragment it reads anyway) and publishes the group's sums; DW = -1 for a
+  // wavefront that owns no row tile.  cnext receives the chunk's offsets c.
+  template <bool FULL, int DW>
   static __device__ __forceinline__ void compute(const W& wc, Lds& L, int buf, int kb, int kb_end,
-                                                 int lane, int wave, f32x4_t (&tot)[MT][NT],
+                                                 int lane, f32x4_t (&tot)[MT][NT],
                                                  float (&cnext)[GPC][NT]) {
+    constexpr int DUTY = DW < 0 ? 0 : (MT - DW + WAVES - 1) / WAVES;
     const int col = lane & 15, quarter = lane >> 4;
     const bf16x8_t ones = __builtin_bit_cast(
         bf16x8_t, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
     const f32x4_t zero = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    int dmt[DUTY];
-#pragma unroll
-    for (int i = 0; i < DUTY; ++i) dmt[i] = (wave + WAVES * i) % MT;
 #pragma unroll
     for (int b = 0; b < CH; ++b) {
-      if (kb + b < kb_end) {
+      if (FULL || kb + b < kb_end) {
         uint32_t pr[NT][16];
 #pragma unroll
         for (int t = 0; t < NT; ++t) unpack_pairs<BITS>(wc.w[b][t], pr[t]);
 #pragma unroll
         for (int gi = 0; gi < GPB; ++gi) {
           const int gc = b * GPB + gi;
-          f32x4_t acc[MT][NT], accx[DUTY];
+          f32x4_t acc[MT][NT], accx[DUTY > 0 ? DUTY : 1];
 #pragma unroll
           for (int js = 0; js < SPG; ++js) {
             const int j = gi * SPG + js;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+            static_for<MT>([&](auto mtc) __attribute__((always_inline)) {
+              constexpr int mt = decltype(mtc)::value;
               const bf16x8_t A = __builtin_bit_cast(
                   bf16x8_t, L.x[buf][slot(16 * mt + col, b, 4 * j + quarter)]);
 #pragma unroll
@@ -412,14 +411,12 @@ struct MfmaBody {
                 acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                     A, B, js == 0 ? zero : acc[mt][t], 0, 0, 0);
               }
-            }
-#pragma unroll
-            for (int i = 0; i < DUTY; ++i) {
-              const bf16x8_t A = __builtin_bit_cast(
-                  bf16x8_t, L.x[buf][slot(16 * dmt[i] + col, b, 4 * j + quarter)]);
-              accx[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, ones, js == 0 ? zero : accx[i],
-                                                                0, 0, 0);
-            }
+              if constexpr (DW >= 0 && mt % WAVES == DW) {
+                constexpr int i = mt / WAVES;
+                accx[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, ones, js == 0 ? zero : accx[i],
+                                                                  0, 0, 0);
+              }
+            });
           }
           float sv[NT];
 #pragma unroll
@@ -431,9 +428,12 @@ struct MfmaBody {
 #pragma unroll
               for (int r = 0; r < 4; ++r) tot[mt][t][r] = __builtin_fmaf(sv[t], acc[mt][t][r], tot[mt][t][r]);
 #pragma unroll
-          for (int i = 0; i < DUTY; ++i)
-            if (wave + WAVES * i < MT && col == 0)
-              *reinterpret_cast<f32x4_t*>(&L.xs[buf][gc][16 * dmt[i] + 4 * quarter]) = accx[i];
+          for (int i = 0; i < DUTY; ++i) {
+            // all 16 columns hold the same sums; lanes of column 0 publish them
+            f32x4_t* dst = col == 0 ? reinterpret_cast<f32x4_t*>(&L.xs[buf][gc][16 * (DW + WAVES * i) + 4 * quarter])
+                                    : &L.sink[lane];
+            *dst = accx[i];
+          }
         }
       }
     }
@@ -486,30 +486,56 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemm_mfma(QArgs a) {
   });
   Body::stage_store(lds, 0, x[0]);
   Body::stage_load(x[0], bu, a.K, kb0 + PF * CH);
+  // The first chunk's zero-point step reads the sums of "chunk -1": zeros, with
+  // zero offsets.
+  for (int i = threadIdx.x; i < GPC * Body::ROWS; i += WAVES * kWave) (&lds.xs[1][0][0])[i] = 0.f;
+#pragma unroll
+  for (int gc = 0; gc < GPC; ++gc)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) cprev[gc][t] = 0.f;
   __syncthreads();
 
-  // One chunk: ring slot U holds chunk c+U; the LDS buffer follows the chunk's parity
-  // (PF is even).  REFILL = false in the drain.
-  auto step = [&](auto u, int c, auto refill) __attribute__((always_inline)) {
-    constexpr int U = decltype(u)::value;
-    constexpr int V = (U + 1) % PF;  // slot of chunk c+U+1
-    const int kb = kb0 + (c + U) * CH;
-    if (c + U > 0) Body::correct(lds, (U + 1) & 1, kb - CH, kb_end, lane, cprev, tot);
-    Body::compute(w[U], lds, U & 1, kb, kb_end, lane, wave, tot, cprev);
-    if constexpr (decltype(refill)::value) Body::load_w(w[U], bu, a, wofs, col, kb + PF * CH);
-    Body::stage_store(lds, (U + 1) & 1, x[V]);
-    if constexpr (decltype(refill)::value) Body::stage_load(x[V], bu, a.K, kb + (PF + 1) * CH);
-    __syncthreads();
+  // The main loop, for a wavefront whose duty is DW (see MfmaBody::compute).
+  auto run = [&](auto dwc) __attribute__((always_inline)) {
+    constexpr int DW = decltype(dwc)::value;
+    // One chunk: ring slot U holds chunk c+U; the LDS buffer follows the chunk's
+    // parity (PF is even).  REFILL = false in the drain.  Every chunk of the steady
+    // state is whole (only the split's last one can be partial), so it runs without
+    // bounds checks.
+    auto step = [&](auto u, int c, auto refill) __attribute__((always_inline)) {
+      constexpr int U = decltype(u)::value;
+      constexpr int V = (U + 1) % PF;  // slot of chunk c+U+1
+      constexpr bool FULL = decltype(refill)::value;
+      const int kb = kb0 + (c + U) * CH;
+      Body::template correct<FULL>(lds, (U + 1) & 1, kb - CH, kb_end, lane, cprev, tot);
+      Body::template compute<FULL, DW>(w[U], lds, U & 1, kb, kb_end, lane, tot, cprev);
+      if constexpr (FULL) Body::load_w(w[U], bu, a, wofs, col, kb + PF * CH);
+      Body::stage_store(lds, (U + 1) & 1, x[V]);
+      if constexpr (FULL) Body::stage_load(x[V], bu, a.K, kb + (PF + 1) * CH);
+      __syncthreads();
+    };
+    // Steady state: straight-line body (every load unconditional) so that each wait
+    // on outstanding loads is exact.  Then drain the last (at most PF) chunks without
+    // further loads, and apply the last chunk's zero-point term.
+    int c = 0;
+    for (; c + PF < nchunks; c += PF)
+      static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::true_type{}); });
+    static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::false_type{}); });
+    Body::template correct<false>(lds, (PF - 1) & 1, kb0 + (c + PF - 1) * CH, kb_end, lane, cprev, tot);
   };
-
-  // Steady state: straight-line body (every load unconditional) so that each wait on
-  // outstanding loads is exact.  Then drain the last (at most PF) chunks without
-  // further loads, and apply the last chunk's zero-point term.
-  int c = 0;
-  for (; c + PF < nchunks; c += PF)
-    static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::true_type{}); });
-  static_for<PF>([&](auto u) __attribute__((always_inline)) { step(u, c, std::false_type{}); });
-  Body::correct(lds, (PF - 1) & 1, kb0 + (c + PF - 1) * CH, kb_end, lane, cprev, tot);
+  // A wavefront's duty is a compile-time property of the code it runs, so the duty
+  // MFMAs reuse the A fragments of the regular ones: one copy of the main loop per
+  // owner wavefront, and one for the wavefronts that own no row tile.
+  if constexpr (MT >= WAVES) {
+    static_for<WAVES>([&](auto wc) __attribute__((always_inline)) {
+      if (wave == decltype(wc)::value) run(wc);
+    });
+  } else {
+    static_for<MT>([&](auto wc) __attribute__((always_inline)) {
+      if (wave == decltype(wc)::value) run(wc);
+    });
+    if (wave >= MT) run(std::integral_constant<int, -1>{});
+  }
 
   // D layout of 16x16 MFMA: lane holds column lane%16, rows 4*(lane/16) + r.
   const int quarter = lane >> 4;
@@ -799,7 +825,10 @@ struct Variant {
   SUBSPEC_MFMA(B, G, 1, 1, 2, 4, 2), SUBSPEC_MFMA(B, G, 1, 2, 2, 4, 2),                       \
       SUBSPEC_MFMA(B, G, 2, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 2, 2, 1, 4, 2),                   \
       SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 4, 2, 1, 4, 4),                   \
-      SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),
+      SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),                   \
+      SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 4), SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 6),                   \
+      SUBSPEC_MFMA(B, G, 2, 1, 1, 4, 4), SUBSPEC_MFMA(B, G, 2, 1, 1, 4, 6),                   \
+      SUBSPEC_MFMA(B, G, 1, 1, 2, 4, 4), SUBSPEC_MFMA(B, G, 1, 1, 1, 4, 8),
 
 static const Variant kVariants[] = {SUBSPEC_BG(SUBSPEC_GEMV_SET) SUBSPEC_BG(SUBSPEC_MFMA_SET)};
 
