@@ -825,10 +825,7 @@ struct Variant {
   SUBSPEC_MFMA(B, G, 1, 1, 2, 4, 2), SUBSPEC_MFMA(B, G, 1, 2, 2, 4, 2),                       \
       SUBSPEC_MFMA(B, G, 2, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 2, 2, 1, 4, 2),                   \
       SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 4, 2, 1, 4, 4),                   \
-      SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),                   \
-      SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 4), SUBSPEC_MFMA(B, G, 4, 1, 1, 4, 6),                   \
-      SUBSPEC_MFMA(B, G, 2, 1, 1, 4, 4), SUBSPEC_MFMA(B, G, 2, 1, 1, 4, 6),                   \
-      SUBSPEC_MFMA(B, G, 1, 1, 2, 4, 4), SUBSPEC_MFMA(B, G, 1, 1, 1, 4, 8),
+      SUBSPEC_MFMA(B, G, 8, 1, 1, 4, 2), SUBSPEC_MFMA(B, G, 8, 2, 1, 4, 2),
 
 static const Variant kVariants[] = {SUBSPEC_BG(SUBSPEC_GEMV_SET) SUBSPEC_BG(SUBSPEC_MFMA_SET)};
 
