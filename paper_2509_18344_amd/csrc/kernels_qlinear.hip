@@ -440,8 +440,18 @@ struct MfmaBody {
   }
 };
 
+// Register budget: with four row tiles and one tile per wavefront the kernel is held
+// to three wavefronts per SIMD (at most 168 VGPRs; left alone the compiler lands on
+// either side of that line), which the planner's residency-aware choices count on.
+// The smaller variants fit four or more by themselves.
+template <int MT, int NT>
+constexpr int mfma_min_waves() {
+  return MT == 4 && NT == 1 ? 3 : 1;
+}
+
 template <int BITS, int GROUP, int MT, int NT, int CH, int WAVES, int PF>
-__global__ __launch_bounds__(WAVES * kWave) void k_qgemm_mfma(QArgs a) {
+__global__ __launch_bounds__(WAVES * kWave) __attribute__((amdgpu_waves_per_eu(mfma_min_waves<MT, NT>())))
+void k_qgemm_mfma(QArgs a) {
   static_assert(PF % 2 == 0, "the LDS buffer of a chunk follows the ring slot's parity");
   using Body = MfmaBody<BITS, GROUP, MT, NT, CH, WAVES>;
   constexpr int GPC = Body::GPC;
