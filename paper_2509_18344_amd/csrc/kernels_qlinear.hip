@@ -252,9 +252,9 @@ struct TileSet {
 // the chunk are kept in registers until then).
 //
 // LDS layout of a chunk: 16-byte pieces, row-major [row][block][piece], the 16
-// pieces of each (row, block) permuted by piece ^ (row & 7).  Copy-in writes eight
-// consecutive pieces of one row per 8 lanes and an A fragment reads one piece of
-// eight consecutive rows per 8 lanes: both touch eight distinct 16-byte bank groups.
+// pieces of each (row, block) permuted by piece ^ (row & 15).  Copy-in writes the 16
+// pieces of one row per 16 lanes and an A fragment reads one piece of 16 consecutive
+// rows per 16 lanes: either way the 16 lanes touch all 64 banks once.
 //
 // All global reads go through buffer resources: 32-bit offsets from a scalar base,
 // and rows past M (offsets past the end of x) read zeros.  Blocks past the split
@@ -301,7 +301,7 @@ struct MfmaBody {
   };
 
   static __device__ __forceinline__ int slot(int row, int b, int piece) {
-    return row * (CH * 16) + b * 16 + (piece ^ (row & 7));
+    return row * (CH * 16) + b * 16 + (piece ^ (row & 15));
   }
 
   // Weights of blocks kb..kb+CH-1 for the wavefront's tiles; wofs[t] is the byte
