@@ -82,10 +82,13 @@ typedef struct subspec_plan {
   int tiles_per_wave;  /* 16-column tiles each wavefront owns                     */
   int waves;           /* wavefronts per workgroup                                */
   int chunk_blocks;    /* 128-k blocks staged in LDS per step                     */
-  int col_groups;      /* workgroups along N                                      */
-  int splits;          /* workgroups along K (split-K); 1 = no partial results    */
+  int col_groups;      /* column groups (waves * tiles_per_wave * 16 columns each) */
+  int full_groups;     /* column groups [0, full_groups) run whole, one workgroup
+                          each; the others are split along K                    */
+  int splits;          /* workgroups per split column group; 1 = no partial sums  */
   int blocks_per_split;/* 128-k blocks per split                                  */
-  int grid;            /* total workgroups = col_groups * splits                  */
+  int grid;            /* total workgroups =
+                          full_groups + (col_groups - full_groups) * splits      */
   size_t workspace_bytes; /* device scratch needed when splits > 1: 64 KiB of
                              completion counters + the splits' fp32 partial sums */
 } subspec_plan;

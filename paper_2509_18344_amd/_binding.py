@@ -27,6 +27,7 @@ class _Plan(ctypes.Structure):
     _fields_ = [("path", ctypes.c_int), ("rows", ctypes.c_int), ("tiles_per_wave", ctypes.c_int),
                 ("waves", ctypes.c_int),
                 ("chunk_blocks", ctypes.c_int), ("col_groups", ctypes.c_int),
+                ("full_groups", ctypes.c_int),
                 ("splits", ctypes.c_int), ("blocks_per_split", ctypes.c_int),
                 ("grid", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t)]
 

@@ -72,6 +72,7 @@ struct Tuning {
   int mfma_ch = 0;
   int mfma_pf = 0;
   int wg_per_cu = 0;              // split-K target workgroups per CU; 0 = path default
+  int tail = 1;                   // split only the column groups past a multiple of the CUs
   int splits = 0;                 // 0 = choose per shape
   int partial_div = 2;            // split-K partial traffic may reach weight bytes / this
 };
@@ -102,6 +103,7 @@ const Tuning& tuning() {
         else if (k == "mfma_ch") r.mfma_ch = v;
         else if (k == "mfma_pf") r.mfma_pf = v;
         else if (k == "wg_per_cu") r.wg_per_cu = v;
+        else if (k == "tail") r.tail = v;
         else if (k == "splits") r.splits = v;
         else if (k == "partial_div") r.partial_div = v;
       }
@@ -229,23 +231,46 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   }
   // Split-K needs a completion counter per column group and 32-bit offsets into the
   // partial sums.
-  if (col_groups > subspec::kSplitCounters) splits = 1;
   const long long split_bytes = 4ll * M * N;
-  if (splits > 1 && split_bytes * splits >= (1ll << 31))
-    splits = std::max(1, static_cast<int>(((1ll << 31) - 1) / split_bytes));
+  auto fit_offsets = [&](int sp) {
+    if (sp > 1 && split_bytes * sp >= (1ll << 31))
+      sp = std::max(1, static_cast<int>(((1ll << 31) - 1) / split_bytes));
+    return sp;
+  };
+  if (col_groups > subspec::kSplitCounters) splits = 1;
+  splits = fit_offsets(splits);
+
+  // Balanced tail.  With col_groups = base * CUs + rem (base >= 1), whole column groups
+  // alone leave rem CUs one group ahead of the rest (592 groups on 256 CUs: 80 CUs run
+  // three, 176 run two).  Instead the first base * CUs groups run whole and the last
+  // rem are split CUs / rem ways, so no CU gets more than base groups plus one part of
+  // a split one.  (A GEMV workgroup that runs a whole group stages all of K.)
+  int full_groups = 0;
+  const int cus = device_cus();
+  if (splits == 1 && tu.tail && !tu.splits && col_groups <= subspec::kSplitCounters &&
+      (c.path != 1 || K <= subspec::gemv_max_kspan(c.rows, c.waves, group, cols_per_group))) {
+    const int base = col_groups / cus, rem = col_groups % cus;
+    const int ts = fit_offsets(std::min(rem ? cus / rem : 0, chunks));
+    if (base >= 1 && ts >= 2) {
+      full_groups = base * cus;
+      splits = ts;
+    }
+  }
   if (splits > chunks) splits = chunks;
   int chunks_per_split = (chunks + splits - 1) / splits;
   const int blocks_per_split = chunks_per_split * c.chunk;
   splits = (KB + blocks_per_split - 1) / blocks_per_split;
+  if (splits == 1) full_groups = 0;
   p->path = path;
   p->rows = c.rows;
   p->tiles_per_wave = c.nt;
   p->waves = c.waves;
   p->chunk_blocks = c.chunk;
   p->col_groups = col_groups;
+  p->full_groups = full_groups;
   p->splits = splits;
   p->blocks_per_split = blocks_per_split;
-  p->grid = col_groups * splits;
+  p->grid = full_groups + (col_groups - full_groups) * splits;
   p->workspace_bytes = 0;
   if (splits > 1)
     p->workspace_bytes = subspec::kSplitCounterBytes + static_cast<size_t>(splits) * M * N * sizeof(float);
@@ -373,8 +398,10 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
   a.K = K;
   a.KB = K / subspec::kTileK;
   a.n_tiles = N / subspec::kTileN;
+  a.full_groups = p.full_groups;
   a.splits = p.splits;
   a.blocks_per_split = p.blocks_per_split;
+  a.span_blocks = p.full_groups > 0 ? a.KB : p.blocks_per_split;
   if (p.splits > 1) {
     void* ws = nullptr;
     rc = get_workspace(p.workspace_bytes, st, &ws);

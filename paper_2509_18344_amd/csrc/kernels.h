@@ -24,8 +24,13 @@ struct QArgs {
   int M, N, K;
   int KB;                 // K / 128
   int n_tiles;            // N / 16
+  // Work assignment: workgroups [0, full_groups) each take one whole column group;
+  // the remaining column groups are split `splits` ways (blocks_per_split 128-k
+  // blocks each), one workgroup per (column group, split).
+  int full_groups;
   int splits;
   int blocks_per_split;
+  int span_blocks;        // largest k-block count of one workgroup (GEMV LDS layout)
 };
 
 struct KernelChoice {

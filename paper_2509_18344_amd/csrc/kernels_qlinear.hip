@@ -157,9 +157,35 @@ __device__ __forceinline__ void scale_and_offset(uint32_t sbits, uint32_t zbits,
 }
 
 // ---------------------------------------------------------------------------
-// Output.  With one split the result goes straight to y.  Otherwise every workgroup
-// stores fp32 partial sums ws[split][m][n], and the last workgroup of its column
-// group to finish adds them in split order and writes y (finish_splitk).  The
+// Work of one workgroup (see QArgs): column group ng, k-blocks [kb0, kb_end), and
+// its split index among the nsplit workgroups of that column group.
+// ---------------------------------------------------------------------------
+
+struct WorkItem {
+  int ng, split, nsplit, kb0, kb_end;
+  __device__ __forceinline__ explicit WorkItem(const QArgs& a) {
+    const int b = blockIdx.x;
+    if (b < a.full_groups) {
+      ng = b;
+      split = 0;
+      nsplit = 1;
+      kb0 = 0;
+      kb_end = a.KB;
+    } else {
+      const int r = b - a.full_groups;
+      ng = a.full_groups + r / a.splits;
+      split = r % a.splits;
+      nsplit = a.splits;
+      kb0 = split * a.blocks_per_split;
+      kb_end = min(a.KB, kb0 + a.blocks_per_split);
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Output.  A workgroup that covers all of K writes y directly.  Otherwise every
+// workgroup of the column group stores fp32 partial sums ws[split][m][n], and the
+// last one to finish adds them in split order and writes y (finish_splitk).  The
 // partial sums are written and read with agent-scope cache policy (coherent across
 // the XCDs' L2 caches) and each workgroup waits for its own stores before counting
 // itself in, so no cache flush or invalidation is needed.
@@ -169,16 +195,18 @@ constexpr int kCachePolicyAgent = 16;  // sc1: coherent at agent scope
 // s_waitcnt vmcnt(0), other counters untouched (expcnt 7, lgkmcnt 15).
 constexpr int kWaitVmcnt0 = 0x0F70;
 
-__device__ __forceinline__ void store_out(const QArgs& a, int split, int m, int n, float v) {
-  if (a.splits == 1)
+__device__ __forceinline__ void store_out(const QArgs& a, const WorkItem& wi, int m, int n, float v) {
+  const int split = wi.split;
+  if (wi.nsplit == 1)
     a.y[static_cast<size_t>(m) * a.N + n] = float_to_bf16_bits(v);
   else
     __hip_atomic_store(a.ws + (static_cast<size_t>(split) * a.M + m) * a.N + n, v, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Split-K completion for column group ng (columns [ng*cols, ng*cols + cols) of N):
-// called by every thread of the workgroup after its partial sums are stored.
+// Split-K completion for column group ng (columns [ng*cols, ng*cols + cols) of N,
+// split a.splits ways): called by every thread of the workgroup after its partial
+// sums are stored.
 template <int THREADS>
 __device__ __forceinline__ void finish_splitk(const QArgs& a, int ng, int cols) {
   __shared__ int last;
@@ -459,9 +487,8 @@ void k_qgemm_mfma(QArgs a) {
 
   const int lane = threadIdx.x % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
-  const int ng = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
-  const int kb0 = split * a.blocks_per_split;
-  const int kb_end = min(a.KB, kb0 + a.blocks_per_split);
+  const WorkItem wi(a);
+  const int ng = wi.ng, kb0 = wi.kb0, kb_end = wi.kb_end;
   const int nchunks = (kb_end - kb0 + CH - 1) / CH;
   const QBuffers bu(a, BITS, GROUP);
 
@@ -556,9 +583,9 @@ void k_qgemm_mfma(QArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = 16 * mt + 4 * quarter + r;
-        if (ok[t] && m < a.M) store_out(a, split, m, col[t], tot[mt][t][r]);
+        if (ok[t] && m < a.M) store_out(a, wi, m, col[t], tot[mt][t][r]);
       }
-  if (a.splits > 1) finish_splitk<WAVES * kWave>(a, ng, WAVES * NT * kTileN);
+  if (wi.nsplit > 1) finish_splitk<WAVES * kWave>(a, ng, WAVES * NT * kTileN);
 }
 
 // ---------------------------------------------------------------------------
@@ -683,12 +710,11 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
 
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   const int quarter = lane >> 4;
-  const int ng = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
-  const int kb0 = split * a.blocks_per_split;
-  const int kb_end = min(a.KB, kb0 + a.blocks_per_split);
+  const WorkItem wi(a);
+  const int ng = wi.ng, kb0 = wi.kb0, kb_end = wi.kb_end;
   const int nblk = kb_end - kb0;
   const int nchunks = (nblk + CH - 1) / CH;
-  const int kspan = a.blocks_per_split * kTileK;
+  const int kspan = a.span_blocks * kTileK;  // LDS layout: the launch's largest span
   const int xs = gemv_x_stride(kspan);
   uint16_t* xl = reinterpret_cast<uint16_t*>(smem);
   float* xsum = reinterpret_cast<float*>(smem + gemv_xsum_offset(ROWS, kspan));
@@ -809,8 +835,8 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
   for (int m = 0; m < ROWS; ++m)
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-      if (ok[t] && (m & 3) == quarter && m < a.M) store_out(a, split, m, col[t], tot[m][t]);
-  if (a.splits > 1) finish_splitk<THREADS>(a, ng, COLS);
+      if (ok[t] && (m & 3) == quarter && m < a.M) store_out(a, wi, m, col[t], tot[m][t]);
+  if (wi.nsplit > 1) finish_splitk<THREADS>(a, ng, COLS);
 }
 
 // ---------------------------------------------------------------------------
@@ -868,7 +894,7 @@ hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QAr
                           hipStream_t st) {
   const Variant* v = find_variant(kc, bits, group);
   if (!v) return hipErrorInvalidDeviceFunction;
-  const size_t lds = kc.path == 1 ? gemv_lds_bytes(kc.rows, a.blocks_per_split * kTileK, group,
+  const size_t lds = kc.path == 1 ? gemv_lds_bytes(kc.rows, a.span_blocks * kTileK, group,
                                                    kc.waves * kc.nt * kTileN)
                                   : 0;
   hipLaunchKernelGGL(v->fn, dim3(grid), dim3(kc.waves * kWave), lds, st, a);

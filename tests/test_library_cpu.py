@@ -103,12 +103,22 @@ def test_plan_choices_are_consistent():
                 assert (p["splits"] - 1) * p["blocks_per_split"] < KB <= p["splits"] * p["blocks_per_split"]
                 cols = p["waves"] * p["tiles_per_wave"] * 16
                 assert p["col_groups"] == -(-N // cols)
-                assert p["grid"] == p["col_groups"] * p["splits"]
+                fg = p["full_groups"]
+                assert 0 <= fg < p["col_groups"]
+                assert p["grid"] == fg + (p["col_groups"] - fg) * p["splits"]
+                if fg:
+                    # whole groups on a multiple of the CUs; the rest split at most
+                    # once per CU
+                    assert p["splits"] > 1 and fg % 256 == 0
+                    assert (p["col_groups"] - fg) * p["splits"] <= 256
                 if p["splits"] == 1:
                     assert p["workspace_bytes"] == 0
                 else:
                     # completion counters (16384 x 4 bytes), then the fp32 partial sums
                     assert p["workspace_bytes"] == 65536 + p["splits"] * M * N * 4
+    # 592 column groups on 256 CUs: 512 whole, the last 80 split three ways
+    p = ss.subspec_qlinear_plan(1, 37888, 3584, 4, 128)
+    assert (p["col_groups"], p["full_groups"], p["splits"], p["grid"]) == (592, 512, 3, 752)
     assert ss.subspec_qlinear_plan(2, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_GEMV
     assert ss.subspec_qlinear_plan(3, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_MFMA
     assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_GEMV)["path"] == ss.SUBSPEC_PATH_GEMV
