@@ -73,6 +73,7 @@ struct Tuning {
   int mfma_pf = 0;
   int wg_per_cu = 0;              // split-K target workgroups per CU; 0 = path default
   int tail = 1;                   // split only the column groups past a multiple of the CUs
+  int fill_cus = 2;               // partial-sum cap still gives each CU this many workgroups
   int splits = 0;                 // 0 = choose per shape
   int partial_div = 2;            // split-K partial traffic may reach weight bytes / this
 };
@@ -104,6 +105,7 @@ const Tuning& tuning() {
         else if (k == "mfma_pf") r.mfma_pf = v;
         else if (k == "wg_per_cu") r.wg_per_cu = v;
         else if (k == "tail") r.tail = v;
+        else if (k == "fill_cus") r.fill_cus = v;
         else if (k == "splits") r.splits = v;
         else if (k == "partial_div") r.partial_div = v;
       }
@@ -222,7 +224,12 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   int splits = std::max(1, target / col_groups);
   const double wbytes = static_cast<double>(N) * K * bits / 8 + 4.0 * N * (K / group);
   const double per_split = 8.0 * M * N;
-  const int cap = std::max(1, static_cast<int>(wbytes / (tu.partial_div * per_split)));
+  int cap = tu.partial_div > 0 ? std::max(1, static_cast<int>(wbytes / (tu.partial_div * per_split)))
+                               : splits;
+  // The cap never leaves a CU with fewer than two workgroups: at large M a
+  // workgroup's own issue rate, not HBM, bounds it, and partial sums cost less than
+  // idle CUs (7B q|k|v at M = 64: 72 workgroups took as long as gate|up).
+  if (tu.fill_cus) cap = std::max(cap, (device_cus() * tu.fill_cus + col_groups - 1) / col_groups);
   splits = std::min(splits, cap);
   if (tu.splits > 0) splits = tu.splits;
   if (c.path == 1) {

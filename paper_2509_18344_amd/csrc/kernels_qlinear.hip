@@ -192,6 +192,7 @@ struct WorkItem {
 // ---------------------------------------------------------------------------
 
 constexpr int kCachePolicyAgent = 16;  // sc1: coherent at agent scope
+constexpr int kFinishBatch = 8;        // partial-sum loads in flight per output quad
 // s_waitcnt vmcnt(0), other counters untouched (expcnt 7, lgkmcnt 15).
 constexpr int kWaitVmcnt0 = 0x0F70;
 
@@ -219,31 +220,53 @@ __device__ __forceinline__ void finish_splitk(const QArgs& a, int ng, int cols) 
   if (!last) return;
   const int n0 = ng * cols;
   const int nq = min(cols, a.N - n0) / 4;  // column quads of the group
+  const int total = a.M * nq;
   const uint32_t split_bytes = static_cast<uint32_t>(a.M) * a.N * 4;
   const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(a.ws, split_bytes * a.splits);
-  for (int q = threadIdx.x; q < a.M * nq; q += THREADS) {
-    const int m = q / nq, n = n0 + 4 * (q % nq);
-    const uint32_t off = (static_cast<uint32_t>(m) * a.N + n) * 4;
-    f32x4_t acc = __builtin_bit_cast(
-        f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ws, off, 0, kCachePolicyAgent));
-    int sp = 1;
-    for (; sp + 3 < a.splits; sp += 4) {  // four loads in flight, added in order
-      f32x4_t v[4];
+  auto load = [&](uint32_t off) __attribute__((always_inline)) {
+    return __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ws, off, 0, kCachePolicyAgent));
+  };
+  // Every read of a partial sum is a trip to the coherent level of the memory
+  // system, so a thread takes two quads at a time and issues the loads of up to
+  // kFinishBatch splits of both before adding them in split order.  Splits past the
+  // last read zeros (an offset past the buffer resource) and leave the sums unchanged.
+  constexpr uint32_t kPastEnd = 0xFFFFFFF0u;
+  for (int q0 = threadIdx.x; q0 < total; q0 += 2 * THREADS) {
+    bool ok[2];
+    int m[2], n[2];
+    uint32_t off[2];
+    f32x4_t acc[2];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        v[u] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                               ws, off + (sp + u) * split_bytes, 0, kCachePolicyAgent));
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc += v[u];
+    for (int i = 0; i < 2; ++i) {
+      const int q = q0 + i * THREADS;
+      ok[i] = q < total;
+      const int qc = ok[i] ? q : q0;
+      m[i] = qc / nq;
+      n[i] = n0 + 4 * (qc % nq);
+      off[i] = (static_cast<uint32_t>(m[i]) * a.N + n[i]) * 4;
+      acc[i] = load(off[i]);
     }
-    for (; sp < a.splits; ++sp)
-      acc += __builtin_bit_cast(
-          f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ws, off + sp * split_bytes, 0, kCachePolicyAgent));
-    const uint32_t lo = static_cast<uint32_t>(float_to_bf16_bits(acc[0])) |
-                        (static_cast<uint32_t>(float_to_bf16_bits(acc[1])) << 16);
-    const uint32_t hi = static_cast<uint32_t>(float_to_bf16_bits(acc[2])) |
-                        (static_cast<uint32_t>(float_to_bf16_bits(acc[3])) << 16);
-    *reinterpret_cast<uint2*>(a.y + static_cast<size_t>(m) * a.N + n) = make_uint2(lo, hi);
+    for (int sp = 1; sp < a.splits; sp += kFinishBatch) {
+      f32x4_t v[2][kFinishBatch];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int u = 0; u < kFinishBatch; ++u)
+          v[i][u] = load(sp + u < a.splits ? off[i] + (sp + u) * split_bytes : kPastEnd);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int u = 0; u < kFinishBatch; ++u) acc[i] += v[i][u];
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (!ok[i]) continue;
+      const uint32_t lo = static_cast<uint32_t>(float_to_bf16_bits(acc[i][0])) |
+                          (static_cast<uint32_t>(float_to_bf16_bits(acc[i][1])) << 16);
+      const uint32_t hi = static_cast<uint32_t>(float_to_bf16_bits(acc[i][2])) |
+                          (static_cast<uint32_t>(float_to_bf16_bits(acc[i][3])) << 16);
+      *reinterpret_cast<uint2*>(a.y + static_cast<size_t>(m[i]) * a.N + n[i]) = make_uint2(lo, hi);
+    }
   }
   if (threadIdx.x == 0) __hip_atomic_store(a.cnt + ng, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
