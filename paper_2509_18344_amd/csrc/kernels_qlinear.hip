@@ -567,8 +567,22 @@ void k_qgemm_mfma(QArgs a) {
       constexpr int V = (U + 1) % PF;  // slot of chunk c+U+1
       constexpr bool FULL = decltype(refill)::value;
       const int kb = kb0 + (c + U) * CH;
-      Body::template correct<FULL>(lds, (U + 1) & 1, kb - CH, kb_end, lane, cprev, tot);
-      Body::template compute<FULL, DW>(w[U], lds, U & 1, kb, kb_end, lane, tot, cprev);
+      if constexpr (MT == 1) {
+        // One row tile: the MFMAs of the chunk go first and the previous chunk's
+        // zero-point term fills their latency (measured faster at M = 8; with more
+        // row tiles the MFMA sequence is long enough on its own, and the order there
+        // is the other way round).
+        float cp[GPC][NT];
+#pragma unroll
+        for (int g = 0; g < GPC; ++g)
+#pragma unroll
+          for (int t = 0; t < NT; ++t) cp[g][t] = cprev[g][t];
+        Body::template compute<FULL, DW>(w[U], lds, U & 1, kb, kb_end, lane, tot, cprev);
+        Body::template correct<FULL>(lds, (U + 1) & 1, kb - CH, kb_end, lane, cp, tot);
+      } else {
+        Body::template correct<FULL>(lds, (U + 1) & 1, kb - CH, kb_end, lane, cprev, tot);
+        Body::template compute<FULL, DW>(w[U], lds, U & 1, kb, kb_end, lane, tot, cprev);
+      }
       if constexpr (FULL) Body::load_w(w[U], bu, a, wofs, col, kb + PF * CH);
       Body::stage_store(lds, (U + 1) & 1, x[V]);
       if constexpr (FULL) Body::stage_load(x[V], bu, a.K, kb + (PF + 1) * CH);
