@@ -70,8 +70,9 @@ enum subspec_status {
 /* Kernel paths (subspec_plan.path, subspec_qlinear_path's `path`). */
 enum subspec_path {
   SUBSPEC_PATH_AUTO = 0, /* let subspec_qlinear_plan choose                        */
-  SUBSPEC_PATH_GEMV = 1, /* VALU dot products, lanes split K, DPP/permlane and LDS
-                            split-K reductions; M <= 8                            */
+  SUBSPEC_PATH_GEMV = 1, /* VALU dot products; the four 16-lane quarters of a
+                            wavefront split K and are summed with lane shuffles,
+                            per-group sums of x reduced with DPP; M <= 8          */
   SUBSPEC_PATH_MFMA = 2  /* bf16 matrix cores on unpacked code tiles; any M        */
 };
 
