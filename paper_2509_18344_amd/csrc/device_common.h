@@ -53,17 +53,22 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uin
                                            kBufferWord3);
 }
 
+// Cache policy of the weight stream: non-temporal (every weight byte is read once per
+// launch), which keeps the activations and scales that are re-read in the caches.
+// Measured on the 7B MLP step: +3-5 % over the default policy.
+constexpr int kStreamPolicy = 2;  // nt
+
 template <int BITS>
 __device__ __forceinline__ Slice<BITS> load_slice(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   Slice<BITS> s;
   if constexpr (BITS == 4) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kStreamPolicy);
     s.w[0] = v[0]; s.w[1] = v[1]; s.w[2] = v[2]; s.w[3] = v[3];
   } else if constexpr (BITS == 2) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kStreamPolicy);
     s.w[0] = v[0]; s.w[1] = v[1];
   } else {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b96(r, off, 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b96(r, off, 0, kStreamPolicy);
     s.w[0] = v[0]; s.w[1] = v[1]; s.w[2] = v[2];
   }
   return s;

@@ -110,43 +110,8 @@ __device__ __forceinline__ void load_spans(SpanRegs<SPT>& r, const QArgs& a, int
 }
 
 // ---------------------------------------------------------------------------
-// Weight stream: every wavefront owns NT tiles (16 columns each) and walks its
-// split's k-blocks in chunks of CH blocks; a ring of PF chunks (slices and raw fp16
-// scale/zero values) is in flight at any time.
+// Dequantization constants.
 // ---------------------------------------------------------------------------
-
-template <int BITS, int NT, int CH, int GPC>
-struct WChunk {
-  Slice<BITS> w[CH][NT];
-  uint32_t s[GPC][NT];  // fp16 bits of the scale
-  uint32_t z[GPC][NT];  // fp16 bits of the zero-point
-};
-
-// Unconditional loads from clamped addresses: blocks past the end of the split
-// re-read its last block and are never consumed.
-template <int BITS, int GROUP, int NT, int CH, int GPC>
-__device__ __forceinline__ void load_wchunk(WChunk<BITS, NT, CH, GPC>& r, const QArgs& a,
-                                            const uint8_t* const (&wbase)[NT],
-                                            const int (&ncol)[NT], int kb, int kb_end) {
-  constexpr int GPB = kTileK / GROUP;
-#pragma unroll
-  for (int b = 0; b < CH; ++b) {
-    const int kbc = min(kb + b, kb_end - 1);
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-      r.w[b][t] = load_slice<BITS>(wbase[t] + static_cast<size_t>(kbc) * (256 * BITS));
-  }
-#pragma unroll
-  for (int gc = 0; gc < GPC; ++gc) {
-    const int g = min(kb * GPB + gc, kb_end * GPB - 1);
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const size_t gi = static_cast<size_t>(g) * a.N + ncol[t];
-      r.s[gc][t] = a.sc[gi];
-      r.z[gc][t] = a.zr[gi];
-    }
-  }
-}
 
 // Per (column, group): the scale s and the offset c = s * (128 + z) that removes the
 // code bias and the zero-point from the group's accumulated x * (128 + q).
@@ -270,23 +235,6 @@ __device__ __forceinline__ void finish_splitk(const QArgs& a, int ng, int cols) 
   }
   if (threadIdx.x == 0) __hip_atomic_store(a.cnt + ng, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-
-// Tile ownership shared by both kernels.
-template <int BITS, int NT>
-struct TileSet {
-  const uint8_t* wbase[NT];
-  bool ok[NT];
-  int ncol[NT];
-  __device__ __forceinline__ TileSet(const QArgs& a, int nt0, int lane) {
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      ok[t] = nt0 + t < a.n_tiles;
-      const int ntc = ok[t] ? nt0 + t : 0;
-      wbase[t] = a.qw + static_cast<size_t>(ntc) * a.KB * (256 * BITS) + lane * (4 * BITS);
-      ncol[t] = ntc * kTileN + (lane & 15);
-    }
-  }
-};
 
 // ---------------------------------------------------------------------------
 // MFMA kernel.  Workgroup = WAVES wavefronts x NT tiles, all rows, one k-split.  Per
