@@ -88,23 +88,24 @@ def test_qlinear_matches_oracle(bits, group, path):
             assert_close(bf16_to_f64(y), y_ref, f"bits={bits} g={group} path={path} M={M} N={N} K={K}")
 
 
-@pytest.mark.parametrize("M", [1, 8, 40, 64])
-def test_qlinear_balanced_tail_split(M):
+@pytest.mark.parametrize("M,bits,group", [(1, 4, 128), (8, 4, 128), (40, 4, 128), (64, 4, 128),
+                                          (2, 3, 128), (16, 3, 64), (5, 2, 64), (100, 2, 128)])
+def test_qlinear_balanced_tail_split(M, bits, group):
     """More column groups than CUs (276 groups of 64 columns): the groups past a
     multiple of the CU count run split along K while the others run whole; every
     output is checked against the oracle."""
-    N, K, bits, group = 16 * 4 * 276, 1024, 4, 128
+    N, K = 16 * 4 * 276, 1024
     plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
     assert 0 < plan["full_groups"] < plan["col_groups"] and plan["splits"] > 1, plan
-    w = _w(N, K, 310, M)
+    w = _w(N, K, 310, M, bits, group)
     p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
     q, s16, z16 = oracle.quantize_minmax(w, bits, group)
-    x = synth.activations(M, K, 311, M)
+    x = synth.activations(M, K, 311, M, bits)
     ss.subspec_reserve(plan["workspace_bytes"])
     for _ in range(2):  # the completion counters must be back at zero for the second call
         y = run_qlinear(p, x.to(DEV))
         y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, group)
-        assert_close(bf16_to_f64(y), y_ref, f"tail split M={M} plan={plan}")
+        assert_close(bf16_to_f64(y), y_ref, f"tail split M={M} bits={bits} g={group} plan={plan}")
 
 
 @pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA])
