@@ -61,17 +61,20 @@ constexpr int kAutoGemvMaxRows = 2;
 
 // --- launch planning --------------------------------------------------------
 
+// Every planning choice below has a default measured on the 7B MLP shapes; the
+// fields exist so that measurement sweeps can override them (SUBSPEC_TUNE).  None of
+// them changes what is computed.
 struct Tuning {
   int gemv_max_m = kAutoGemvMaxRows;  // largest M the automatic plan sends to the GEMV path
-  int target_blocks = 0;          // workgroups to aim for; 0 = one full residency round
-  int gemv_nt = 1;
-  int gemv_waves = 4;
+  int target_blocks = 0;          // workgroups to aim for; 0 = the per-CU target below
+  int gemv_nt = 1;                // tiles per GEMV wavefront
+  int gemv_waves = 4;             // wavefronts per GEMV workgroup
   int gemv_ch = 0;                // 128-k blocks per GEMV ring stage; 0 = choose per M
   int gemv_pf = 0;                // ring depth in stages; 0 = the variant's
   int mfma_nt = 0;                // tiles per MFMA wavefront; 0 = choose per shape
-  int mfma_ch = 0;
-  int mfma_pf = 0;
-  int wg_per_cu = 0;              // split-K target workgroups per CU; 0 = path default
+  int mfma_ch = 0;                // 128-k blocks per MFMA chunk; 0 = choose per M
+  int mfma_pf = 0;                // MFMA ring depth in chunks; 0 = the variant's
+  int wg_per_cu = 0;              // split-K target workgroups per CU; 0 = two
   int tail = 1;                   // split only the column groups past a multiple of the CUs
   int fill_cus = 2;               // partial-sum cap still gives each CU this many workgroups
   int splits = 0;                 // 0 = choose per shape
