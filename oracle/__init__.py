@@ -1,4 +1,5 @@
-"""Plain fp64 CPU oracle for the low-bit substitute-layer linear (SubSpec, Sec. 4.1).
+"""Plain fp64 CPU oracle for the low-bit substitute-layer linear (SubSpec, Sec. 4.1)
+and for the draft-tree expansion step with probability sharpening (Sec. 4.2, App. D).
 
 TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import or call anything in this package.
@@ -20,4 +21,10 @@ from .qlinear import (  # noqa: F401
     unpack,
     qlinear_ref,
     qlinear_ref_cols,
+)
+from .tree import (  # noqa: F401
+    log_softmax_rows,
+    expand_scores,
+    tree_expand,
+    kth_gap,
 )
