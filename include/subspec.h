@@ -192,6 +192,33 @@ int subspec_graph_launch(subspec_graph* graph, hipStream_t stream);
 /* Release a captured sequence (synchronous with respect to its replays). */
 int subspec_graph_destroy(subspec_graph* graph);
 
+/* Draft-tree expansion with probability sharpening (Sec. 4.2 "Constructing Deep
+ * Context-Aware Dynamic Draft Tree" and "Draft Probability Sharpening", App. D): after
+ * a draft pass, leaf i of the tree has logits l_i over the vocabulary and a path
+ * score s_i.  Every candidate (leaf i, token v) scores
+ *     score(i, v) = s_i + log softmax(l_i / T)(v)
+ * -- the logarithm of the product of the parent's path score and the sharpened
+ * conditional probability (the paper uses T = 0.2 for greedy decoding; path scores
+ * are carried as natural logarithms, 0 at the root) -- and the k best candidates
+ * over all leaves are the next leaves.  Order: larger score first, ties broken by
+ * the smaller flat index i * V + v.  fp32 arithmetic; every reduction in a fixed
+ * order, so repeated calls give identical results.
+ *   logits       device bf16 [R][V] row-major, finite values, 16-byte aligned
+ *   parent_logp  device fp32 [R]: s_i
+ *   parent_out   device int32 [k]: leaf index i of each winner, best first
+ *   token_out    device int32 [k]: token v
+ *   score_out    device fp32 [k]: score(i, v)
+ * Needs 1 <= R <= 1024, V a positive multiple of 8, R * V < 2^31, 1 <= k <= 32,
+ * k <= R * V, T > 0 and 1/T finite.  Uses the library's per-device workspace
+ * (subspec_tree_workspace_bytes bytes; see subspec_reserve); like subspec_qlinear,
+ * calls that overlap in time on one device must be serialised. */
+int subspec_tree_expand(const void* logits, const float* parent_logp, int R, int V,
+                        float temperature, int k, int* parent_out, int* token_out,
+                        float* score_out, hipStream_t stream);
+
+/* Workspace bytes subspec_tree_expand needs for (R, V, k); 0 on bad arguments. */
+size_t subspec_tree_workspace_bytes(int R, int V, int k);
+
 /* Grow the calling device's workspace to at least `bytes` now (synchronous, may
  * call hipMalloc), so that later calls, e.g. under stream capture, need not. */
 int subspec_reserve(size_t bytes);

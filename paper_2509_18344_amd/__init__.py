@@ -1,4 +1,5 @@
-"""MI355X (gfx950) low-bit substitute layers of SubSpec (Sec. 4.1).
+"""MI355X (gfx950) low-bit substitute layers of SubSpec (Sec. 4.1), and the draft-tree
+expansion step that follows every draft pass (Sec. 4.2).
 
 The compute path is the native library ``libsubspec.so`` (hand-written HIP,
 C ABI in ``include/subspec.h``); this package only marshals arguments to it.
@@ -26,4 +27,6 @@ from ._binding import (  # noqa: F401
     subspec_stack_capture,
     subspec_graph_launch,
     subspec_graph_destroy,
+    subspec_tree_expand,
+    subspec_tree_workspace_bytes,
 )

@@ -71,6 +71,8 @@ def load_library():
                                       ctypes.POINTER(ctypes.c_void_p)]),
         "subspec_graph_launch": (I, [P, P]),
         "subspec_graph_destroy": (I, [P]),
+        "subspec_tree_expand": (I, [P, P, I, I, ctypes.c_float, I, P, P, P, P]),
+        "subspec_tree_workspace_bytes": (S, [I, I, I]),
         "subspec_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -194,3 +196,14 @@ def subspec_graph_launch(graph, stream=None) -> int:
 
 def subspec_graph_destroy(graph) -> int:
     return _check("subspec_graph_destroy", load_library().subspec_graph_destroy(graph))
+
+
+def subspec_tree_expand(logits, parent_logp, R, V, temperature, k, parent_out, token_out,
+                        score_out, stream=None) -> int:
+    return _check("subspec_tree_expand", load_library().subspec_tree_expand(
+        _ptr(logits), _ptr(parent_logp), R, V, float(temperature), k, _ptr(parent_out),
+        _ptr(token_out), _ptr(score_out), _stream(stream)))
+
+
+def subspec_tree_workspace_bytes(R, V, k) -> int:
+    return int(load_library().subspec_tree_workspace_bytes(R, V, k))

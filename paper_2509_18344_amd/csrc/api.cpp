@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -578,6 +579,57 @@ int subspec_graph_destroy(subspec_graph* g) {
   if (e1 != hipSuccess) return hip_fail(e1, "hipDeviceSynchronize");
   if (e2 != hipSuccess) return hip_fail(e2, "hipGraphExecDestroy");
   if (e3 != hipSuccess) return hip_fail(e3, "hipGraphDestroy");
+  return SUBSPEC_OK;
+}
+
+size_t subspec_tree_workspace_bytes(int R, int V, int k) {
+  if (R < 1 || R > subspec::kTreeMaxRows || V < 8 || V % 8 || k < 1 || k > subspec::kTreeMaxK)
+    return 0;
+  return subspec::tree_workspace_bytes(R, V, k);
+}
+
+int subspec_tree_expand(const void* logits, const float* parent_logp, int R, int V,
+                        float temperature, int k, int* parent_out, int* token_out,
+                        float* score_out, hipStream_t stream) {
+  if (!logits || !parent_logp || !parent_out || !token_out || !score_out)
+    return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (!aligned16(logits)) return fail(SUBSPEC_EINVAL, "logits must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(parent_logp) | reinterpret_cast<uintptr_t>(parent_out) |
+       reinterpret_cast<uintptr_t>(token_out) | reinterpret_cast<uintptr_t>(score_out)) & 3u)
+    return fail(SUBSPEC_EINVAL, "scores and outputs must be 4-byte aligned");
+  if (R < 1 || R > subspec::kTreeMaxRows)
+    return fail(SUBSPEC_EUNSUPPORTED, "R=%d: must be in 1..%d", R, subspec::kTreeMaxRows);
+  if (V < 8 || V % 8) return fail(SUBSPEC_EUNSUPPORTED, "V=%d: must be a positive multiple of 8", V);
+  if (static_cast<long long>(R) * V >= (1ll << 31))
+    return fail(SUBSPEC_EUNSUPPORTED, "R*V=%lld: must be below 2^31", static_cast<long long>(R) * V);
+  if (k < 1 || k > subspec::kTreeMaxK || static_cast<long long>(k) > static_cast<long long>(R) * V)
+    return fail(SUBSPEC_EUNSUPPORTED, "k=%d: must be in 1..%d and at most R*V", k, subspec::kTreeMaxK);
+  if (!(temperature > 0.f) || !std::isfinite(temperature) || !std::isfinite(1.f / temperature))
+    return fail(SUBSPEC_EINVAL, "temperature must be positive and finite");
+  void* ws = nullptr;
+  const int rc = get_workspace(subspec::tree_workspace_bytes(R, V, k), stream, &ws);
+  if (rc) return rc;
+  subspec::TreeArgs a{};
+  a.logits = static_cast<const uint16_t*>(logits);
+  a.parent = parent_logp;
+  a.R = R;
+  a.V = V;
+  a.k = k;
+  a.inv_t = 1.f / temperature;
+  subspec::tree_plan(R, V, &a.chunks, &a.chunk_len);
+  const size_t blocks = static_cast<size_t>(R) * a.chunks;
+  char* base = static_cast<char*>(ws);
+  a.cnt = reinterpret_cast<unsigned*>(base);
+  char* p = base + subspec::kSplitCounterBytes;
+  a.stat_m = reinterpret_cast<float*>(p);
+  a.stat_s = a.stat_m + blocks;
+  a.cand_val = a.stat_s + blocks;
+  a.cand_idx = reinterpret_cast<int*>(a.cand_val + blocks * k);
+  a.out_parent = parent_out;
+  a.out_token = token_out;
+  a.out_score = score_out;
+  const hipError_t e = subspec::launch_tree_expand(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "tree_expand launch");
   return SUBSPEC_OK;
 }
 

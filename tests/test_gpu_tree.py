@@ -1,0 +1,104 @@
+"""GPU parity of the draft-tree expansion kernel against the fp64 oracle, through the C
+ABI.  Scores are compared with |s - s_ref| <= 2e-4 + 1e-6 |s_ref| (fp32 against fp64:
+z = l / T reaches ~75 at T = 0.2 and the log-sum-exp cancels against it); the
+selection is compared exactly wherever the oracle's k-th and (k+1)-th candidates are
+further apart than that, and otherwise checked for validity (every winner is within
+tolerance of the oracle's k-th score, no duplicates, best first)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2509_18344_amd as ss
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+ATOL, RTOL = 2e-4, 1e-6
+
+
+def _logits(R, V, seed, scale=3.0):
+    rng = np.random.default_rng(seed)
+    return oracle.bf16_round_bits(rng.normal(0.0, scale, (R, V)).astype(np.float32))
+
+
+def _run(bits, parent, T, k):
+    R, V = bits.shape
+    lg = torch.from_numpy(bits.view(np.int16)).to(DEV)
+    pr = torch.from_numpy(np.asarray(parent, dtype=np.float32)).to(DEV)
+    po = torch.empty(k, dtype=torch.int32, device=DEV)
+    to = torch.empty(k, dtype=torch.int32, device=DEV)
+    so = torch.empty(k, dtype=torch.float32, device=DEV)
+    ss.subspec_tree_expand(lg, pr, R, V, T, k, po, to, so)
+    torch.cuda.synchronize()
+    return po.cpu().numpy(), to.cpu().numpy(), so.cpu().numpy()
+
+
+def _check(bits, parent, T, k, what):
+    pi, tok, sc = _run(bits, parent, T, k)
+    ref_pi, ref_tok, ref_sc = oracle.tree_expand(bits, np.asarray(parent, np.float32).astype(np.float64), T, k)
+    s_all = oracle.expand_scores(bits, np.asarray(parent, np.float32).astype(np.float64), T)
+    R, V = bits.shape
+    assert ((pi >= 0) & (pi < R) & (tok >= 0) & (tok < V)).all(), what
+    assert len(set(zip(pi.tolist(), tok.tolist()))) == k, what
+    assert (np.diff(sc) <= 0).all(), what
+    mine = s_all[pi, tok]
+    assert np.all(np.abs(sc - mine) <= ATOL + RTOL * np.abs(mine)), (what, sc, mine)
+    assert np.all(mine >= ref_sc[-1] - 2 * ATOL), what
+    gap = oracle.kth_gap(bits, np.asarray(parent, np.float32).astype(np.float64), T, k)
+    if gap > 4 * ATOL:
+        assert set(zip(pi.tolist(), tok.tolist())) == set(zip(ref_pi.tolist(), ref_tok.tolist())), what
+    return pi, tok, sc
+
+
+@pytest.mark.parametrize("R,V,k,T", [(1, 8, 1, 0.2), (1, 8, 8, 0.2), (6, 1000, 6, 0.2),
+                                     (6, 152064, 6, 0.2), (6, 152064, 6, 1.0), (37, 4096, 17, 0.2),
+                                     (128, 152064, 6, 0.2), (3, 2048, 32, 0.5), (1024, 64, 32, 0.2)])
+def test_tree_expand_matches_oracle(R, V, k, T):
+    bits = _logits(R, V, 1000 + R + V + k)
+    parent = np.random.default_rng(R * 7 + k).uniform(-12.0, 0.0, R)
+    _check(bits, parent, T, k, f"R={R} V={V} k={k} T={T}")
+
+
+def test_tree_expand_ties_follow_flat_index():
+    R, V, k = 4, 4096, 10
+    bits = np.full((R, V), oracle.bf16_round_bits(np.float32(1.25)), dtype=np.uint16)
+    parent = np.array([-1.0, -0.5, -0.5, -3.0], dtype=np.float32)
+    pi, tok, _ = _run(bits, parent, 0.2, k)
+    # rows 1 and 2 tie everywhere; the smaller flat index wins, so row 1 fills all k
+    assert list(pi) == [1] * k and list(tok) == list(range(k))
+
+
+def test_tree_expand_peaked_rows_and_depth():
+    # a few dominant tokens per row, as after sharpening: winners come from the best
+    # parents' dominant tokens, scores follow the parents
+    R, V, k = 6, 152064, 6
+    rng = np.random.default_rng(5)
+    x = rng.normal(0.0, 1.0, (R, V)).astype(np.float32)
+    for i in range(R):
+        x[i, rng.integers(0, V, 3)] += np.float32(12.0)
+    bits = oracle.bf16_round_bits(x)
+    parent = np.array([-0.1, -4.0, -0.3, -9.0, -0.2, -2.5], dtype=np.float32)
+    _check(bits, parent, 0.2, k, "peaked")
+
+
+def test_tree_expand_deterministic_and_reuses_workspace():
+    bits = _logits(6, 152064, 9)
+    parent = np.zeros(6, np.float32)
+    a = _run(bits, parent, 0.2, 6)
+    for _ in range(3):
+        b = _run(bits, parent, 0.2, 6)
+        for u, w in zip(a, b):
+            assert np.array_equal(u, w)
+
+
+def test_tree_expand_chained_passes():
+    # three draft passes: each pass's winners become the next pass's leaves, with
+    # their scores as parent scores (the cumulative product in the log domain)
+    R, V, k = 6, 32768, 6
+    parent = np.zeros(R, np.float32)
+    for depth in range(3):
+        bits = _logits(R, V, 40 + depth)
+        pi, tok, sc = _check(bits, parent, 0.2, k, f"depth {depth}")
+        assert np.all(sc <= parent.max() + ATOL)
+        parent = sc.astype(np.float32)

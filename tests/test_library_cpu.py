@@ -143,3 +143,21 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_binding, "_HERE", str(tmp_path))
     with pytest.raises(RuntimeError, match="missing"):
         _binding.load_library()
+
+
+def test_tree_expand_argument_errors_need_no_gpu():
+    # (R, V, k, T): rejected before any GPU work
+    for R, V, k, T, err in [(0, 64, 1, 0.2, "EUNSUPPORTED"), (1025, 64, 1, 0.2, "EUNSUPPORTED"),
+                            (2, 100, 1, 0.2, "EUNSUPPORTED"), (2, 64, 0, 0.2, "EUNSUPPORTED"),
+                            (2, 64, 33, 0.2, "EUNSUPPORTED"), (1, 8, 9, 0.2, "EUNSUPPORTED"),
+                            (2, 64, 4, 0.0, "EINVAL"), (2, 64, 4, -1.0, "EINVAL"),
+                            (1000, 1 << 22, 4, 0.2, "EUNSUPPORTED")]:
+        with pytest.raises(ss.SubspecError) as ei:
+            ss.subspec_tree_expand(16, 16, R, V, T, k, 16, 16, 16, stream=0)
+        assert err in str(ei.value), (R, V, k, T)
+    with pytest.raises(ss.SubspecError):
+        ss.subspec_tree_expand(None, 16, 2, 64, 0.2, 4, 16, 16, 16, stream=0)
+    with pytest.raises(ss.SubspecError):
+        ss.subspec_tree_expand(24, 16, 2, 64, 0.2, 4, 16, 16, 16, stream=0)
+    assert ss.subspec_tree_workspace_bytes(6, 152064, 6) > 65536
+    assert ss.subspec_tree_workspace_bytes(6, 100, 6) == 0
