@@ -49,7 +49,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen7b_mlp")
+    ap.add_argument("--workload", default="qwen7b_mlp",
+                    help="qwen7b_mlp (default), qwen7b_stack, qwen32b_stack, qwen32b_2bit, tiny, "
+                         "or tree_expand (the draft-tree expansion step; --ms gives its rows)")
     ap.add_argument("--ms", default=None, help="comma-separated M values (default: the workload's)")
     ap.add_argument("--rotate-gb", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -453,6 +455,9 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n}))
         return
     ss.load_library()
+    if args.workload == "tree_expand":
+        run_tree(args, torch, ss)
+        return
     wl = WORKLOADS[args.workload]
     ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else wl.ms
     stream = torch.cuda.Stream()
@@ -510,6 +515,111 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, ms)
+    line = json.dumps(out)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(line + "\n")
+    print(line, flush=True)
+
+
+# --- draft-tree expansion (Sec. 4.2, App. D) --------------------------------------
+
+TREE_V = 152064      # Qwen2.5 vocabulary
+TREE_K = 6           # leaves kept per draft pass (Sec. 5.1)
+TREE_T = 0.2         # draft temperature for greedy decoding (Sec. 4.2, App. D)
+
+
+def tree_cpu_baseline(rs, min_seconds=10.0):
+    """Time the fp64 oracle on the same expansion inputs until `min_seconds` pass."""
+    import oracle
+    rng = np.random.default_rng(3)
+    cases = [(oracle.bf16_round_bits(rng.normal(0, 3, (R, TREE_V)).astype(np.float32)),
+              rng.uniform(-12, 0, R)) for R in rs]
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        for bits, parent in cases:
+            oracle.tree_expand(bits, parent, TREE_T, TREE_K)
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    nbytes = steps * sum(2 * R * TREE_V for R in rs)
+    return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "seconds": round(dt, 3),
+            "sample": f"{steps} pass(es) of the expansion at R in {list(rs)}, V={TREE_V}, "
+                      f"k={TREE_K}, T={TREE_T} (NumPy fp64, one thread)"}
+
+
+def run_tree(args, torch, ss):
+    """One step = one expansion per R (leaves of the tree) over V = 152064 bf16 logits,
+    logits rotating over >= --rotate-gb of distinct copies (they sit in HBM, not in the
+    last-level cache, when a call starts)."""
+    rs = tuple(int(m) for m in args.ms.split(",")) if args.ms else (TREE_K,)
+    stream = torch.cuda.Stream()
+    rng = np.random.default_rng(3)
+    sets = []
+    for R in rs:
+        per = 2 * R * TREE_V
+        copies = max(2, int(math.ceil(args.rotate_gb * 1e9 / per)))
+        base = torch.from_numpy(rng.normal(0, 3, (R, TREE_V)).astype(np.float32)).to("cuda").bfloat16()
+        lg = [base.roll(c, dims=1).contiguous() for c in range(copies)]
+        parent = torch.from_numpy(rng.uniform(-12, 0, R).astype(np.float32)).to("cuda")
+        out = (torch.empty(TREE_K, dtype=torch.int32, device="cuda"),
+               torch.empty(TREE_K, dtype=torch.int32, device="cuda"),
+               torch.empty(TREE_K, dtype=torch.float32, device="cuda"))
+        sets.append((R, lg, parent, out))
+    ss.subspec_reserve(max(ss.subspec_tree_workspace_bytes(R, TREE_V, TREE_K) for R in rs))
+    torch.cuda.synchronize()
+
+    def call(R, lg, parent, out, s):
+        ss.subspec_tree_expand(lg[s % len(lg)], parent, R, TREE_V, TREE_T, TREE_K, out[0], out[1],
+                               out[2], stream)
+
+    def step(s):
+        for (R, lg, parent, out) in sets:
+            call(R, lg, parent, out, s)
+
+    with torch.cuda.stream(stream):
+        total_ms = timed(torch, stream, step, args.warmup, args.steps)
+        per_launch = []
+        for (R, lg, parent, out) in sets:
+            ev = []
+            for r in range(max(args.per_launch_reps, len(lg))):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                call(R, lg, parent, out, r)
+                e1.record(stream)
+                ev.append((e0, e1))
+            torch.cuda.synchronize()
+            t = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3
+            nbytes = 2 * R * TREE_V + 4 * R + 12 * TREE_K
+            per_launch.append({"R": R, "V": TREE_V, "k": TREE_K, "avg_us": round(float(t.mean()), 2),
+                               "p10_us": round(float(np.percentile(t, 10)), 2),
+                               "alg_bytes": nbytes,
+                               "alg_GBs": round(nbytes / (t.mean() * 1e-6) / 1e9, 1)})
+    ms_per_step = total_ms / args.steps
+    step_bytes = sum(2 * R * TREE_V for R in rs)
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    dom = max(per_launch, key=lambda d: d["avg_us"])
+    out = {
+        "metric": "logits GB/s of the draft-tree expansion step (sharpened log-softmax, parent "
+                  "scores, global top-k)",
+        "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic: N(0,3) bf16 logits, U(-12,0) parent scores, seeded",
+        "config": {"workload": f"draft-tree expansion, V={TREE_V}, k={TREE_K}, T={TREE_T}",
+                   "rows": list(rs), "launches_per_step": len(rs), "timing": "eager launches"},
+        "roofline": {"bound": "hbm", "achieved": dom["alg_GBs"], "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(dom["alg_GBs"] / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": f"k_tree_expand (R={dom['R']})",
+                     "avg_us": dom["avg_us"], "alg_bytes_per_launch": dom["alg_bytes"]},
+        "per_launch": per_launch,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = tree_cpu_baseline(rs)
     line = json.dumps(out)
     if args.json_out:
         with open(args.json_out, "w") as f:

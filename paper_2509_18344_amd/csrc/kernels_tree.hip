@@ -7,7 +7,7 @@
 // score first, then the smaller flat index i * V + v.
 //
 // One launch, two phases.  Workgroup (row i, chunk c) streams its slice of l_i once
-// (16-byte loads of eight bf16 logits), keeping per thread an online softmax pair
+// (16-byte loads of eight bf16 logits, four loads in flight per thread), keeping per thread an online softmax pair
 // (running max m, sum of exp(z - m)) and a sorted list of its k best z = l / T; the
 // workgroup merges both and stores them.  The last workgroup to finish (completion
 // counter, as in the qlinear split-K) combines the pairs of each row into its
@@ -25,6 +25,10 @@ namespace {
 
 constexpr int kTreeThreads = 256;
 constexpr int kTreeWaves = kTreeThreads / kWave;
+constexpr int kTreeMaxBlocks = 1024;  // R * chunks never exceeds this (tree_plan)
+constexpr int kTreeBatch = 16;        // candidate loads in flight per thread
+constexpr int kTreeLoads = 4;         // logit loads in flight per thread
+constexpr int kTreeCoherent = 16;     // sc1: coherent at agent scope
 
 // Candidate order: larger value first, then smaller index.
 __device__ __forceinline__ bool better(float av, int ai, float bv, int bi) {
@@ -85,7 +89,53 @@ struct TreeShared {
   float bv[kTreeWaves];
   int bi[kTreeWaves];
   int last;
+  // the k winners of the workgroup, stored to memory after the last round (a store
+  // inside a round would make every following barrier wait for it)
+  float win_v[kTreeMaxK];
+  int win_i[kTreeMaxK];
 };
+
+// One step of a wavefront reduction over (value, index) with a DPP lane move.  Rows
+// outside ROW_MASK keep their own pair (the move returns it as `old`).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void dpp_best(float& v, int& i) {
+  const int vb = __builtin_bit_cast(int, v);
+  const float ov = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(vb, vb, CTRL, ROW_MASK, 0xF, false));
+  const int oi = __builtin_amdgcn_update_dpp(i, i, CTRL, ROW_MASK, 0xF, false);
+  if (better(ov, oi, v, i)) {
+    v = ov;
+    i = oi;
+  }
+}
+
+// The wavefront's best (value, index) in every lane: quads, half rows and rows by
+// lane permutations, then rows 0-1 and 2-3 by row broadcasts into lane 63.
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+  dpp_best<0xB1, 0xF>(v, i);   // quad_perm [1,0,3,2]
+  dpp_best<0x4E, 0xF>(v, i);   // quad_perm [2,3,0,1]
+  dpp_best<0x141, 0xF>(v, i);  // row_half_mirror
+  dpp_best<0x140, 0xF>(v, i);  // row_mirror
+  dpp_best<0x142, 0xA>(v, i);  // row_bcast:15 into rows 1 and 3
+  dpp_best<0x143, 0xC>(v, i);  // row_bcast:31 into rows 2 and 3
+  v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), kWave - 1));
+  i = __builtin_amdgcn_readlane(i, kWave - 1);
+}
+
+// Largest value over the wavefront (same lane moves), in every lane.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_max_step(float v) {
+  const int vb = __builtin_bit_cast(int, v);
+  return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(vb, vb, CTRL, ROW_MASK, 0xF, false)));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = dpp_max_step<0xB1, 0xF>(v);
+  v = dpp_max_step<0x4E, 0xF>(v);
+  v = dpp_max_step<0x141, 0xF>(v);
+  v = dpp_max_step<0x140, 0xF>(v);
+  v = dpp_max_step<0x142, 0xA>(v);
+  v = dpp_max_step<0x143, 0xC>(v);
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), kWave - 1));
+}
 
 // Workgroup-wide best head of the threads' lists, removed from its owner; k rounds
 // give the workgroup's k best in order.  All threads get (value, index).
@@ -93,15 +143,7 @@ template <int KMAX>
 __device__ __forceinline__ void take_best(TopList<KMAX>& t, TreeShared& sh, float& val, int& idx) {
   float v = t.v[0];
   int i = t.i[0];
-#pragma unroll
-  for (int off = kWave / 2; off >= 1; off >>= 1) {
-    const float ov = __shfl_xor(v, off);
-    const int oi = __shfl_xor(i, off);
-    if (better(ov, oi, v, i)) {
-      v = ov;
-      i = oi;
-    }
-  }
+  wave_best(v, i);
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   if (lane == 0) {
     sh.bv[wave] = v;
@@ -124,30 +166,65 @@ template <int KMAX>
 __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
   __shared__ TreeShared sh;
   __shared__ float lse_row[kTreeMaxRows];
+  __shared__ float stat_lds[2 * kTreeMaxBlocks];
   const int blk = blockIdx.x;
   const int row = blk / a.chunks, ch = blk % a.chunks;
   const int v0 = ch * a.chunk_len, v1 = min(a.V, v0 + a.chunk_len);
 
   // Phase 1: this workgroup's slice of row `row`.
-  const uint16_t* lrow = a.logits + static_cast<size_t>(row) * a.V;
+  // kTreeLoads 16-byte loads per thread are in flight before any is used; loads
+  // past the chunk read zeros (buffer resource ends at v1) and are skipped.
+  const __amdgpu_buffer_rsrc_t lr = buffer_rsrc(a.logits + static_cast<size_t>(row) * a.V, v1 * 2);
   float m = -INFINITY, s = 0.f;
   TopList<KMAX> top;
   top.clear();
-  for (int v = v0 + static_cast<int>(threadIdx.x) * 8; v < v1; v += kTreeThreads * 8) {
-    const u32x4_t q = *reinterpret_cast<const u32x4_t*>(lrow + v);
+  // theta: the largest KMAX-th best over the lanes.  That lane already holds KMAX
+  // values >= theta, so nothing below theta can be among the wavefront's k best;
+  // raising it once per batch keeps the (divergent) insertions rare.
+  float theta = -INFINITY;
+  // The trip count is the same for every lane (wave_max needs all lanes active);
+  // each lane skips the logits past the chunk.
+  for (int vb0 = v0; vb0 < v1; vb0 += kTreeThreads * 8 * kTreeLoads) {
+    const int vb = vb0 + static_cast<int>(threadIdx.x) * 8;
+    u32x4_t q[kTreeLoads];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t w = q[e / 2];
-      const float x = __uint_as_float(e % 2 ? (w & 0xFFFF0000u) : (w << 16));  // bf16 -> f32
-      const float z = x * a.inv_t;
-      if (z > m) {
-        s = s * __expf(m - z) + 1.f;
-        m = z;
-      } else {
-        s += __expf(z - m);
+    for (int u = 0; u < kTreeLoads; ++u)
+      q[u] = __builtin_amdgcn_raw_buffer_load_b128(lr, static_cast<uint32_t>(vb + u * kTreeThreads * 8) * 2,
+                                                   0, 0);
+#pragma unroll
+    for (int u = 0; u < kTreeLoads; ++u) {
+      const int v = vb + u * kTreeThreads * 8;
+      if (v >= v1) continue;
+      float z[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t w = q[u][e / 2];
+        z[e] = __uint_as_float(e % 2 ? (w & 0xFFFF0000u) : (w << 16)) * a.inv_t;  // bf16 -> f32
       }
-      top.insert(z, v + e);
+      // online softmax over the eight: one rescale per load
+      float m8 = z[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) m8 = fmaxf(m8, z[e]);
+      const float mn = fmaxf(m, m8);
+      float add = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) add += __expf(z[e] - mn);
+      s = (m == -INFINITY ? 0.f : s * __expf(m - mn)) + add;
+      m = mn;
+      // the rare logits at or above theta go through one insertion site
+      unsigned hit = 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) hit |= (z[e] >= theta ? 1u : 0u) << e;
+      while (hit) {
+        const int e = __builtin_ctz(hit);
+        hit &= hit - 1;
+        float ze = z[0];
+#pragma unroll
+        for (int f = 1; f < 8; ++f) ze = e == f ? z[f] : ze;
+        if (better(ze, v + e, top.v[KMAX - 1], top.i[KMAX - 1])) top.insert(ze, v + e);
+      }
     }
+    theta = wave_max(top.v[KMAX - 1]);
   }
   // (m, s) over the workgroup: lanes, then wavefronts, in a fixed order.
 #pragma unroll
@@ -170,11 +247,15 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
     int idx;
     take_best(top, sh, val, idx);
     if (threadIdx.x == 0) {
-      __hip_atomic_store(a.cand_val + static_cast<size_t>(blk) * a.k + j, val, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(a.cand_idx + static_cast<size_t>(blk) * a.k + j, idx, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      sh.win_v[j] = val;
+      sh.win_i[j] = idx;
     }
+  }
+  __syncthreads();
+  if (static_cast<int>(threadIdx.x) < a.k) {
+    const size_t o = static_cast<size_t>(blk) * a.k + threadIdx.x;
+    __hip_atomic_store(a.cand_val + o, sh.win_v[threadIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(a.cand_idx + o, sh.win_i[threadIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (threadIdx.x == 0) {
     __hip_atomic_store(a.stat_m + blk, bm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -190,35 +271,95 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
   __syncthreads();
   if (!sh.last) return;
 
-  // Phase 2: log-sum-exp of every row from its chunks' pairs, in chunk order.
+  // Phase 2.  The workgroups' results are read with the coherent cache policy; each
+  // read is a trip to the coherent level of the memory system, so the (m, s) pairs
+  // and the first batch of candidates are all requested before anything waits.
+  const int nblk = gridDim.x;
+  const int per_row = a.chunks * a.k;
+  const int total = a.R * per_row;
+  const __amdgpu_buffer_rsrc_t rm_ = buffer_rsrc(a.stat_m, nblk * 4);
+  const __amdgpu_buffer_rsrc_t rs_ = buffer_rsrc(a.stat_s, nblk * 4);
+  const __amdgpu_buffer_rsrc_t rv_ = buffer_rsrc(a.cand_val, total * 4);
+  const __amdgpu_buffer_rsrc_t ri_ = buffer_rsrc(a.cand_idx, total * 4);
+  float z[kTreeBatch];
+  int v[kTreeBatch];
+  auto load_batch = [&](int q0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < kTreeBatch; ++u) {  // past the end: zeros, skipped when used
+      const uint32_t off = static_cast<uint32_t>(q0 + u * kTreeThreads) * 4;
+      z[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rv_, off, 0, kTreeCoherent));
+      v[u] = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(ri_, off, 0, kTreeCoherent));
+    }
+  };
+  float pm[kTreeMaxBlocks / kTreeThreads], ps[kTreeMaxBlocks / kTreeThreads];
+#pragma unroll
+  for (int u = 0; u < kTreeMaxBlocks / kTreeThreads; ++u) {
+    const uint32_t off = static_cast<uint32_t>(threadIdx.x + u * kTreeThreads) * 4;
+    pm[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rm_, off, 0, kTreeCoherent));
+    ps[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs_, off, 0, kTreeCoherent));
+  }
+  load_batch(threadIdx.x);
+#pragma unroll
+  for (int u = 0; u < kTreeMaxBlocks / kTreeThreads; ++u) {
+    const int q = threadIdx.x + u * kTreeThreads;
+    if (q < nblk) {
+      stat_lds[2 * q] = pm[u];
+      stat_lds[2 * q + 1] = ps[u];
+    }
+  }
+  __syncthreads();
+  // The log-sum-exp of every row from its chunks' pairs, in chunk order.
   for (int r = threadIdx.x; r < a.R; r += kTreeThreads) {
     float rm = -INFINITY, rs = 0.f;
     for (int c = 0; c < a.chunks; ++c)
-      softmax_merge(rm, rs,
-                    __hip_atomic_load(a.stat_m + r * a.chunks + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
-                    __hip_atomic_load(a.stat_s + r * a.chunks + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      softmax_merge(rm, rs, stat_lds[2 * (r * a.chunks + c)], stat_lds[2 * (r * a.chunks + c) + 1]);
     lse_row[r] = rm + __logf(rs);
   }
   __syncthreads();
   // Every stored candidate becomes a score; the k best over all rows are the result.
   top.clear();
-  const int per_row = a.chunks * a.k;
-  for (int q = threadIdx.x; q < a.R * per_row; q += kTreeThreads) {
-    const int r = q / per_row;
-    const float z = __hip_atomic_load(a.cand_val + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int v = __hip_atomic_load(a.cand_idx + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (v == INT_MAX) continue;  // an empty slot of a chunk shorter than k
-    top.insert(a.parent[r] + (z - lse_row[r]), r * a.V + v);
+  for (int q0 = threadIdx.x; q0 < total; q0 += kTreeThreads * kTreeBatch) {
+    if (q0 != static_cast<int>(threadIdx.x)) load_batch(q0);
+    // scores of the batch, then one insertion site for the valid ones
+    float sc[kTreeBatch];
+    unsigned ok = 0;
+#pragma unroll
+    for (int u = 0; u < kTreeBatch; ++u) {
+      const int q = q0 + u * kTreeThreads;
+      const bool valid = q < total && v[u] != INT_MAX;  // past the end, or an empty slot
+      const int r = valid ? q / per_row : 0;
+      sc[u] = a.parent[r] + (z[u] - lse_row[r]);
+      v[u] = r * a.V + v[u];
+      ok |= (valid ? 1u : 0u) << u;
+    }
+    while (ok) {
+      const int u = __builtin_ctz(ok);
+      ok &= ok - 1;
+      float su = sc[0];
+      int iu = v[0];
+#pragma unroll
+      for (int w = 1; w < kTreeBatch; ++w) {
+        su = u == w ? sc[w] : su;
+        iu = u == w ? v[w] : iu;
+      }
+      top.insert(su, iu);
+    }
   }
   for (int j = 0; j < a.k; ++j) {
     float val;
     int idx;
     take_best(top, sh, val, idx);
     if (threadIdx.x == 0) {
-      a.out_parent[j] = idx / a.V;
-      a.out_token[j] = idx % a.V;
-      a.out_score[j] = val;
+      sh.win_v[j] = val;
+      sh.win_i[j] = idx;
     }
+  }
+  __syncthreads();
+  if (static_cast<int>(threadIdx.x) < a.k) {
+    const int idx = sh.win_i[threadIdx.x];
+    a.out_parent[threadIdx.x] = idx / a.V;
+    a.out_token[threadIdx.x] = idx % a.V;
+    a.out_score[threadIdx.x] = sh.win_v[threadIdx.x];
   }
   if (threadIdx.x == 0) __hip_atomic_store(a.cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -226,7 +367,8 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
 }  // namespace
 
 void tree_plan(int R, int V, int* chunks, int* chunk_len) {
-  // About two workgroups per CU of the 256, at least 2048 logits each.
+  // About two workgroups per CU of the 256, at least 2048 logits (one 16-byte load
+  // per thread) each.
   int c = (512 + R - 1) / R;
   const int cmax = (V + 2047) / 2048;
   if (c > cmax) c = cmax;
