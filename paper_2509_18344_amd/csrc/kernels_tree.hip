@@ -29,6 +29,7 @@ constexpr int kTreeMaxBlocks = 1024;  // R * chunks never exceeds this (tree_pla
 constexpr int kTreeBatch = 16;        // candidate loads in flight per thread
 constexpr int kTreeLoads = 4;         // logit loads in flight per thread
 constexpr int kTreeCoherent = 16;     // sc1: coherent at agent scope
+constexpr int kTreeCap = 2048;        // candidates ranked at once in LDS
 
 // Candidate order: larger value first, then smaller index.
 __device__ __forceinline__ bool better(float av, int ai, float bv, int bi) {
@@ -86,9 +87,12 @@ __device__ __forceinline__ void softmax_merge(float& m, float& s, float m2, floa
 
 struct TreeShared {
   float wm[kTreeWaves], ws[kTreeWaves];
-  float bv[kTreeWaves];
-  int bi[kTreeWaves];
+  // per-wavefront heads of a selection round; rounds alternate between the two
+  // slots, so one barrier per round suffices
+  float bv[2][kTreeWaves];
+  int bi[2][kTreeWaves];
   int last;
+  int n;  // candidates appended to the LDS buffer
   // the k winners of the workgroup, stored to memory after the last round (a store
   // inside a round would make every following barrier wait for it)
   float win_v[kTreeMaxK];
@@ -137,29 +141,159 @@ __device__ __forceinline__ float wave_max(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), kWave - 1));
 }
 
-// Workgroup-wide best head of the threads' lists, removed from its owner; k rounds
-// give the workgroup's k best in order.  All threads get (value, index).
+// Workgroup-wide best head of the threads' lists, removed from its owner; rounds
+// 0..k-1 give the workgroup's k best in order.  All threads get (value, index).
+// A thread can write the slot of round j + 2 only after every thread has reached
+// the barrier of round j + 1, i.e. has finished reading round j.
 template <int KMAX>
-__device__ __forceinline__ void take_best(TopList<KMAX>& t, TreeShared& sh, float& val, int& idx) {
+__device__ __forceinline__ void take_best(TopList<KMAX>& t, TreeShared& sh, int round, float& val, int& idx) {
   float v = t.v[0];
   int i = t.i[0];
   wave_best(v, i);
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int slot = round & 1;
   if (lane == 0) {
-    sh.bv[wave] = v;
-    sh.bi[wave] = i;
+    sh.bv[slot][wave] = v;
+    sh.bi[slot][wave] = i;
   }
   __syncthreads();
-  val = sh.bv[0];
-  idx = sh.bi[0];
+  val = sh.bv[slot][0];
+  idx = sh.bi[slot][0];
 #pragma unroll
   for (int w = 1; w < kTreeWaves; ++w)
-    if (better(sh.bv[w], sh.bi[w], val, idx)) {
-      val = sh.bv[w];
-      idx = sh.bi[w];
+    if (better(sh.bv[slot][w], sh.bi[slot][w], val, idx)) {
+      val = sh.bv[slot][w];
+      idx = sh.bi[slot][w];
+    }
+  if (t.i[0] == idx) t.pop();
+}
+
+// The k-th largest (1 <= k <= 8) of eight values: a 19-comparator sorting network
+// (descending), then a pick.
+__device__ __forceinline__ float kth_of8(const float (&z)[8], int k) {
+  float a[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) a[e] = z[e];
+  constexpr int net[19][2] = {{0, 1}, {2, 3}, {4, 5}, {6, 7}, {0, 2}, {1, 3}, {4, 6}, {5, 7}, {1, 2}, {5, 6},
+                              {0, 4}, {3, 7}, {1, 5}, {2, 6}, {1, 4}, {3, 6}, {2, 4}, {3, 5}, {3, 4}};
+#pragma unroll
+  for (int c = 0; c < 19; ++c) {
+    const float hi = fmaxf(a[net[c][0]], a[net[c][1]]), lo = fminf(a[net[c][0]], a[net[c][1]]);
+    a[net[c][0]] = hi;
+    a[net[c][1]] = lo;
+  }
+  // sorted: the k-th largest is the smallest of the first k (a pick by index would
+  // be compiled into an indexed load from memory)
+  float r = a[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) r = e < k ? fminf(r, a[e]) : r;
+  return r;
+}
+
+// A value that at least k of the lanes' heads reach: the largest heads are taken off
+// round by round (tied lanes together) until k are counted; -inf if the wavefront
+// holds fewer than k finite heads.  Called with every lane active.
+__device__ __forceinline__ float wave_kth_head(float h, int k) {
+  float th = -INFINITY;
+  int cnt = 0;
+  while (cnt < k) {
+    const float mx = wave_max(h);
+    if (mx == -INFINITY) return -INFINITY;
+    cnt += __popcll(__ballot(h == mx));
+    th = mx;
+    h = h == mx ? -INFINITY : h;
+  }
+  return th;
+}
+
+struct Cand {
+  float v;
+  int i;
+};
+
+// The k best of the n (<= kTreeCap) buffered candidates, by rank: each candidate
+// counts the candidates better than it (indices are distinct, so ranks are too) and
+// the ranks below k take their places; places past n get empty entries.  Ends with
+// a barrier.
+// The buffer is read two entries per 16-byte load and compared without branches, so
+// the loads of an unrolled step are all in flight together.
+__device__ __forceinline__ int better01(float av, int ai, float bv, int bi) {
+  return static_cast<int>(av > bv) | (static_cast<int>(av == bv) & static_cast<int>(ai < bi));
+}
+__device__ __forceinline__ void rank_select(const Cand* buf, int n, int k, TreeShared& sh) {
+  const int n2 = n & ~1;
+  for (int c = threadIdx.x; c < n; c += kTreeThreads) {
+    const Cand me = buf[c];
+    int r = 0;
+#pragma unroll 4
+    for (int j = 0; j < n2; j += 2) {
+      const float4 w = *reinterpret_cast<const float4*>(buf + j);
+      r += better01(w.x, __float_as_int(w.y), me.v, me.i) + better01(w.z, __float_as_int(w.w), me.v, me.i);
+    }
+    if (n & 1) r += better01(buf[n - 1].v, buf[n - 1].i, me.v, me.i);
+    if (r < k) {
+      sh.win_v[r] = me.v;
+      sh.win_i[r] = me.i;
+    }
+  }
+  for (int t = threadIdx.x; t < k; t += kTreeThreads)
+    if (t >= n) {
+      sh.win_v[t] = -INFINITY;
+      sh.win_i[t] = INT_MAX;
     }
   __syncthreads();
-  if (t.i[0] == idx) t.pop();
+}
+
+// The k best entries of the threads' lists into sh.win_v / sh.win_i, best first.
+// A threshold that some wavefront's heads reach k times leaves few entries; those
+// are ranked in LDS.  If more than kTreeCap remain (ties), k rounds of take_best.
+// Called with every thread active; ends with a barrier.
+template <int KMAX>
+__device__ __forceinline__ void select_from_lists(TopList<KMAX>& top, TreeShared& sh, Cand* buf, int k) {
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const float th = wave_kth_head(top.v[0], k);
+  if (lane == 0) sh.bv[0][wave] = th;
+  if (threadIdx.x == 0) sh.n = 0;
+  __syncthreads();
+  float theta = sh.bv[0][0];
+#pragma unroll
+  for (int w = 1; w < kTreeWaves; ++w) theta = fmaxf(theta, sh.bv[0][w]);
+  // the entries at or above theta are a prefix of each sorted list
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) cnt += top.i[j] != INT_MAX && top.v[j] >= theta ? 1 : 0;
+  int off = 0;
+  if (cnt) off = atomicAdd(&sh.n, cnt);
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j)
+    if (j < cnt && off + j < kTreeCap) buf[off + j] = Cand{top.v[j], top.i[j]};
+  __syncthreads();
+  const int n = sh.n;
+  if (n <= kTreeCap) {
+    rank_select(buf, n, k, sh);
+    return;
+  }
+  for (int j = 0; j < k; ++j) {
+    float val;
+    int idx;
+    take_best(top, sh, j, val, idx);
+    if (threadIdx.x == 0) {
+      sh.win_v[j] = val;
+      sh.win_i[j] = idx;
+    }
+  }
+  __syncthreads();
+}
+
+// The k-th entry of a sorted list (k <= KMAX): the smallest of the first k, which
+// keeps the list in registers (a pick by index would be compiled into an indexed
+// load from memory).
+template <int KMAX>
+__device__ __forceinline__ float kth_entry(const TopList<KMAX>& t, int k) {
+  float r = t.v[0];
+#pragma unroll
+  for (int j = 1; j < KMAX; ++j) r = j < k ? fminf(r, t.v[j]) : r;
+  return r;
 }
 
 template <int KMAX>
@@ -167,6 +301,8 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
   __shared__ TreeShared sh;
   __shared__ float lse_row[kTreeMaxRows];
   __shared__ float stat_lds[2 * kTreeMaxBlocks];
+  __shared__ float par_lds[kTreeMaxRows];
+  __shared__ __align__(16) Cand cbuf[kTreeCap];
   const int blk = blockIdx.x;
   const int row = blk / a.chunks, ch = blk % a.chunks;
   const int v0 = ch * a.chunk_len, v1 = min(a.V, v0 + a.chunk_len);
@@ -178,9 +314,11 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
   float m = -INFINITY, s = 0.f;
   TopList<KMAX> top;
   top.clear();
-  // theta: the largest KMAX-th best over the lanes.  That lane already holds KMAX
-  // values >= theta, so nothing below theta can be among the wavefront's k best;
-  // raising it once per batch keeps the (divergent) insertions rare.
+  // theta: a value such that some lane has seen k values >= theta (its list keeps
+  // them), so nothing below theta can be among the wavefront's k best.  It starts
+  // from the largest k-th best of the lanes' first eight logits (k <= 8) and is
+  // raised from the lanes' lists once per batch; the (divergent) insertions of the
+  // logits at or above it stay rare.
   float theta = -INFINITY;
   // The trip count is the same for every lane (wave_max needs all lanes active);
   // each lane skips the logits past the chunk.
@@ -194,13 +332,16 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
 #pragma unroll
     for (int u = 0; u < kTreeLoads; ++u) {
       const int v = vb + u * kTreeThreads * 8;
-      if (v >= v1) continue;
+      const bool live = v < v1;
       float z[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const uint32_t w = q[u][e / 2];
         z[e] = __uint_as_float(e % 2 ? (w & 0xFFFF0000u) : (w << 16)) * a.inv_t;  // bf16 -> f32
       }
+      if (KMAX == 8 && theta == -INFINITY)  // wave-uniform: the first load with live lanes
+        theta = wave_max(live ? kth_of8(z, a.k) : -INFINITY);
+      if (!live) continue;
       // online softmax over the eight: one rescale per load
       float m8 = z[0];
 #pragma unroll
@@ -224,7 +365,7 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
         if (better(ze, v + e, top.v[KMAX - 1], top.i[KMAX - 1])) top.insert(ze, v + e);
       }
     }
-    theta = wave_max(top.v[KMAX - 1]);
+    theta = fmaxf(theta, wave_max(kth_entry(top, a.k)));
   }
   // (m, s) over the workgroup: lanes, then wavefronts, in a fixed order.
 #pragma unroll
@@ -241,17 +382,7 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
   float bm = sh.wm[0], bs = sh.ws[0];
 #pragma unroll
   for (int w = 1; w < kTreeWaves; ++w) softmax_merge(bm, bs, sh.wm[w], sh.ws[w]);
-  __syncthreads();
-  for (int j = 0; j < a.k; ++j) {
-    float val;
-    int idx;
-    take_best(top, sh, val, idx);
-    if (threadIdx.x == 0) {
-      sh.win_v[j] = val;
-      sh.win_i[j] = idx;
-    }
-  }
-  __syncthreads();
+  select_from_lists(top, sh, cbuf, a.k);
   if (static_cast<int>(threadIdx.x) < a.k) {
     const size_t o = static_cast<size_t>(blk) * a.k + threadIdx.x;
     __hip_atomic_store(a.cand_val + o, sh.win_v[threadIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -291,70 +422,151 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
       v[u] = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(ri_, off, 0, kTreeCoherent));
     }
   };
-  float pm[kTreeMaxBlocks / kTreeThreads], ps[kTreeMaxBlocks / kTreeThreads];
+  constexpr int kPer = kTreeMaxBlocks / kTreeThreads;
+  static_assert(kTreeMaxRows <= kTreeMaxBlocks, "one parent score per block slot");
+  const __amdgpu_buffer_rsrc_t rp_ = buffer_rsrc(a.parent, a.R * 4);
+  float pm[kPer], ps[kPer], pk[kPer], ph[kPer], pp[kPer];  // per block: (m, s), k-th and first candidate; parents
 #pragma unroll
-  for (int u = 0; u < kTreeMaxBlocks / kTreeThreads; ++u) {
-    const uint32_t off = static_cast<uint32_t>(threadIdx.x + u * kTreeThreads) * 4;
+  for (int u = 0; u < kPer; ++u) {
+    const int b = threadIdx.x + u * kTreeThreads;
+    const uint32_t off = static_cast<uint32_t>(b) * 4;
     pm[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rm_, off, 0, kTreeCoherent));
     ps[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs_, off, 0, kTreeCoherent));
+    pk[u] = __uint_as_float(
+        __builtin_amdgcn_raw_buffer_load_b32(rv_, static_cast<uint32_t>(b * a.k + a.k - 1) * 4, 0, kTreeCoherent));
+    ph[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rv_, static_cast<uint32_t>(b * a.k) * 4, 0, kTreeCoherent));
+    pp[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rp_, off, 0, 0));
   }
   load_batch(threadIdx.x);
 #pragma unroll
-  for (int u = 0; u < kTreeMaxBlocks / kTreeThreads; ++u) {
+  for (int u = 0; u < kPer; ++u) {
     const int q = threadIdx.x + u * kTreeThreads;
     if (q < nblk) {
       stat_lds[2 * q] = pm[u];
       stat_lds[2 * q + 1] = ps[u];
     }
+    if (q < a.R) par_lds[q] = pp[u];
+  }
+  if (threadIdx.x == 0) sh.n = 0;
+  __syncthreads();
+  // The log-sum-exp of every row from its chunks' pairs: a group of G lanes per row
+  // (G the power of two >= chunks, at most a wavefront), each lane over chunks
+  // lane, lane + G, ..., then a butterfly over the group.  Both merges of a
+  // butterfly pair give the same bits, so every lane ends with the same pair.
+  {
+    int G = 1;
+    while (G < a.chunks && G < kWave) G <<= 1;
+    const int rows_per_pass = kTreeThreads / G;
+    const int gl = threadIdx.x % G, gi = threadIdx.x / G;
+    for (int r0 = 0; r0 < a.R; r0 += rows_per_pass) {  // the same trip count for all lanes
+      const int r = r0 + gi;
+      float rm = -INFINITY, rs = 0.f;
+      if (r < a.R)
+        for (int c = gl; c < a.chunks; c += G)
+          softmax_merge(rm, rs, stat_lds[2 * (r * a.chunks + c)], stat_lds[2 * (r * a.chunks + c) + 1]);
+      for (int off = 1; off < G; off <<= 1) {
+        const float om = __shfl_xor(rm, off), os = __shfl_xor(rs, off);
+        softmax_merge(rm, rs, om, os);
+      }
+      if (r < a.R && gl == 0) lse_row[r] = rm + __logf(rs);
+    }
   }
   __syncthreads();
-  // The log-sum-exp of every row from its chunks' pairs, in chunk order.
-  for (int r = threadIdx.x; r < a.R; r += kTreeThreads) {
-    float rm = -INFINITY, rs = 0.f;
-    for (int c = 0; c < a.chunks; ++c)
-      softmax_merge(rm, rs, stat_lds[2 * (r * a.chunks + c)], stat_lds[2 * (r * a.chunks + c) + 1]);
-    lse_row[r] = rm + __logf(rs);
+  // theta: a score that k candidates reach, so nothing below it can be among the k
+  // best: the best score of any block's k-th candidate (that block alone has k
+  // candidates at or above it: a score grows with z within a row, also in rounding),
+  // or a value that k lanes' best block heads reach, whichever is larger.
+  {
+    float tb = -INFINITY, hb = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int b = threadIdx.x + u * kTreeThreads;
+      if (b < nblk) {
+        const int r = b / a.chunks;
+        tb = fmaxf(tb, par_lds[r] + (pk[u] - lse_row[r]));
+        hb = fmaxf(hb, par_lds[r] + (ph[u] - lse_row[r]));
+      }
+    }
+    tb = fmaxf(wave_max(tb), wave_kth_head(hb, a.k));
+    if (lane == 0) sh.wm[wave] = tb;
   }
   __syncthreads();
-  // Every stored candidate becomes a score; the k best over all rows are the result.
-  top.clear();
-  for (int q0 = threadIdx.x; q0 < total; q0 += kTreeThreads * kTreeBatch) {
-    if (q0 != static_cast<int>(threadIdx.x)) load_batch(q0);
-    // scores of the batch, then one insertion site for the valid ones
-    float sc[kTreeBatch];
+  float theta2 = sh.wm[0];
+#pragma unroll
+  for (int w = 1; w < kTreeWaves; ++w) theta2 = fmaxf(theta2, sh.wm[w]);
+  // Every stored candidate becomes a score; those at or above theta are kept.
+  float sc[kTreeBatch];
+  auto score_batch = [&](int q0) __attribute__((always_inline)) -> unsigned {
     unsigned ok = 0;
 #pragma unroll
     for (int u = 0; u < kTreeBatch; ++u) {
       const int q = q0 + u * kTreeThreads;
       const bool valid = q < total && v[u] != INT_MAX;  // past the end, or an empty slot
       const int r = valid ? q / per_row : 0;
-      sc[u] = a.parent[r] + (z[u] - lse_row[r]);
+      sc[u] = par_lds[r] + (z[u] - lse_row[r]);
       v[u] = r * a.V + v[u];
-      ok |= (valid ? 1u : 0u) << u;
+      ok |= (valid && sc[u] >= theta2 ? 1u : 0u) << u;
     }
-    while (ok) {
-      const int u = __builtin_ctz(ok);
-      ok &= ok - 1;
-      float su = sc[0];
-      int iu = v[0];
+    return ok;
+  };
+  auto pick = [&](int u, float& su, int& iu) __attribute__((always_inline)) {
+    su = sc[0];
+    iu = v[0];
 #pragma unroll
-      for (int w = 1; w < kTreeBatch; ++w) {
-        su = u == w ? sc[w] : su;
-        iu = u == w ? v[w] : iu;
-      }
-      top.insert(su, iu);
+    for (int w = 1; w < kTreeBatch; ++w) {
+      su = u == w ? sc[w] : su;
+      iu = u == w ? v[w] : iu;
     }
-  }
-  for (int j = 0; j < a.k; ++j) {
-    float val;
-    int idx;
-    take_best(top, sh, val, idx);
-    if (threadIdx.x == 0) {
-      sh.win_v[j] = val;
-      sh.win_i[j] = idx;
+  };
+  // Usually only a few candidates reach theta: they go to the LDS buffer and are
+  // ranked there.
+  for (int q0 = threadIdx.x; q0 < total; q0 += kTreeThreads * kTreeBatch) {
+    if (q0 != static_cast<int>(threadIdx.x)) load_batch(q0);
+    unsigned ok = score_batch(q0);
+    if (ok) {
+      int off = atomicAdd(&sh.n, __popc(ok));
+      while (ok) {
+        const int u = __builtin_ctz(ok);
+        ok &= ok - 1;
+        float su;
+        int iu;
+        pick(u, su, iu);
+        if (off < kTreeCap) cbuf[off] = Cand{su, iu};
+        ++off;
+      }
     }
   }
   __syncthreads();
+  const int n = sh.n;
+  if (n <= kTreeCap) {
+    rank_select(cbuf, n, a.k, sh);
+  } else {
+    // More ties than the buffer holds: the same candidates again, through the
+    // threads' lists and k rounds of take_best.
+    top.clear();
+    for (int q0 = threadIdx.x; q0 < total; q0 += kTreeThreads * kTreeBatch) {
+      load_batch(q0);
+      unsigned ok = score_batch(q0);
+      while (ok) {
+        const int u = __builtin_ctz(ok);
+        ok &= ok - 1;
+        float su;
+        int iu;
+        pick(u, su, iu);
+        top.insert(su, iu);
+      }
+    }
+    for (int j = 0; j < a.k; ++j) {
+      float val;
+      int idx;
+      take_best(top, sh, j, val, idx);
+      if (threadIdx.x == 0) {
+        sh.win_v[j] = val;
+        sh.win_i[j] = idx;
+      }
+    }
+    __syncthreads();
+  }
   if (static_cast<int>(threadIdx.x) < a.k) {
     const int idx = sh.win_i[threadIdx.x];
     a.out_parent[threadIdx.x] = idx / a.V;

@@ -69,6 +69,17 @@ def test_tree_expand_ties_follow_flat_index():
     assert list(pi) == [1] * k and list(tok) == list(range(k))
 
 
+def test_tree_expand_ties_beyond_the_candidate_buffer():
+    # every logit and parent equal: more tied candidates than the ranking buffer holds
+    # in both the per-chunk and the final selection, which then take the round-based
+    # path; ties go to the smallest flat indices, i.e. row 0's first k tokens
+    R, V, k = 16, 152064, 32
+    bits = np.full((R, V), oracle.bf16_round_bits(np.float32(-0.75)), dtype=np.uint16)
+    pi, tok, sc = _run(bits, np.full(R, -2.0, np.float32), 0.2, k)
+    assert list(pi) == [0] * k and list(tok) == list(range(k))
+    assert np.allclose(sc, -2.0 - np.log(V), atol=ATOL)
+
+
 def test_tree_expand_peaked_rows_and_depth():
     # a few dominant tokens per row, as after sharpening: winners come from the best
     # parents' dominant tokens, scores follow the parents
