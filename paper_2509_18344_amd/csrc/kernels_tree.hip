@@ -168,28 +168,6 @@ __device__ __forceinline__ void take_best(TopList<KMAX>& t, TreeShared& sh, int 
   if (t.i[0] == idx) t.pop();
 }
 
-// The k-th largest (1 <= k <= 8) of eight values: a 19-comparator sorting network
-// (descending), then a pick.
-__device__ __forceinline__ float kth_of8(const float (&z)[8], int k) {
-  float a[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) a[e] = z[e];
-  constexpr int net[19][2] = {{0, 1}, {2, 3}, {4, 5}, {6, 7}, {0, 2}, {1, 3}, {4, 6}, {5, 7}, {1, 2}, {5, 6},
-                              {0, 4}, {3, 7}, {1, 5}, {2, 6}, {1, 4}, {3, 6}, {2, 4}, {3, 5}, {3, 4}};
-#pragma unroll
-  for (int c = 0; c < 19; ++c) {
-    const float hi = fmaxf(a[net[c][0]], a[net[c][1]]), lo = fminf(a[net[c][0]], a[net[c][1]]);
-    a[net[c][0]] = hi;
-    a[net[c][1]] = lo;
-  }
-  // sorted: the k-th largest is the smallest of the first k (a pick by index would
-  // be compiled into an indexed load from memory)
-  float r = a[0];
-#pragma unroll
-  for (int e = 1; e < 8; ++e) r = e < k ? fminf(r, a[e]) : r;
-  return r;
-}
-
 // A value that at least k of the lanes' heads reach: the largest heads are taken off
 // round by round (tied lanes together) until k are counted; -inf if the wavefront
 // holds fewer than k finite heads.  Called with every lane active.
@@ -285,17 +263,6 @@ __device__ __forceinline__ void select_from_lists(TopList<KMAX>& top, TreeShared
   __syncthreads();
 }
 
-// The k-th entry of a sorted list (k <= KMAX): the smallest of the first k, which
-// keeps the list in registers (a pick by index would be compiled into an indexed
-// load from memory).
-template <int KMAX>
-__device__ __forceinline__ float kth_entry(const TopList<KMAX>& t, int k) {
-  float r = t.v[0];
-#pragma unroll
-  for (int j = 1; j < KMAX; ++j) r = j < k ? fminf(r, t.v[j]) : r;
-  return r;
-}
-
 template <int KMAX>
 __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
   __shared__ TreeShared sh;
@@ -314,11 +281,11 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
   float m = -INFINITY, s = 0.f;
   TopList<KMAX> top;
   top.clear();
-  // theta: a value such that some lane has seen k values >= theta (its list keeps
-  // them), so nothing below theta can be among the wavefront's k best.  It starts
-  // from the largest k-th best of the lanes' first eight logits (k <= 8) and is
-  // raised from the lanes' lists once per batch; the (divergent) insertions of the
-  // logits at or above it stay rare.
+  // theta: a value that k of the logits seen by the wavefront reach (the lists keep
+  // them), so nothing below it can be among the wavefront's k best.  It is set from
+  // the k-th largest of the lanes' maxima of their first eight logits and raised once
+  // per batch from the k-th largest of the lanes' list heads; the (divergent)
+  // insertions of the logits at or above it stay rare.
   float theta = -INFINITY;
   // The trip count is the same for every lane (wave_max needs all lanes active);
   // each lane skips the logits past the chunk.
@@ -339,13 +306,13 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
         const uint32_t w = q[u][e / 2];
         z[e] = __uint_as_float(e % 2 ? (w & 0xFFFF0000u) : (w << 16)) * a.inv_t;  // bf16 -> f32
       }
-      if (KMAX == 8 && theta == -INFINITY)  // wave-uniform: the first load with live lanes
-        theta = wave_max(live ? kth_of8(z, a.k) : -INFINITY);
-      if (!live) continue;
-      // online softmax over the eight: one rescale per load
       float m8 = z[0];
 #pragma unroll
       for (int e = 1; e < 8; ++e) m8 = fmaxf(m8, z[e]);
+      if (theta == -INFINITY)  // wave-uniform: until a first bound is found
+        theta = wave_kth_head(live ? m8 : -INFINITY, a.k);
+      if (!live) continue;
+      // online softmax over the eight: one rescale per load
       const float mn = fmaxf(m, m8);
       float add = 0.f;
 #pragma unroll
@@ -365,7 +332,7 @@ __global__ __launch_bounds__(kTreeThreads) void k_tree_expand(TreeArgs a) {
         if (better(ze, v + e, top.v[KMAX - 1], top.i[KMAX - 1])) top.insert(ze, v + e);
       }
     }
-    theta = fmaxf(theta, wave_max(kth_entry(top, a.k)));
+    theta = fmaxf(theta, wave_kth_head(top.v[0], a.k));
   }
   // (m, s) over the workgroup: lanes, then wavefronts, in a fixed order.
 #pragma unroll
