@@ -20,8 +20,12 @@ bounded sample.
 
 ``--summarize-pmc FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR`` turns four
 rocprofv3 ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` runs (of this script and of its
-``--copy-calibration-mb`` copy) into profiles/traffic.json, which later runs read
-for ``roofline.traffic`` while the kernel sources are unchanged.
+``--copy-calibration-mb`` copy) into profiles/traffic.json (with ``--workload
+tree_expand``: profiles/traffic_tree.json), which later runs read for
+``roofline.traffic`` while that kernel family's sources are unchanged.
+
+``--workload tree_expand`` times the draft-tree expansion step instead (sharpened
+log-softmax of R x 152064 bf16 logits, parent scores, global top-6).
 """
 from __future__ import annotations
 
@@ -41,7 +45,16 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
-TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic.json")
+# Per kernel family: where its measured traffic is kept, which sources it depends on
+# and which kernel names belong to it.
+FAMILIES = {
+    "qlinear": {"json": os.path.join(ROOT, "profiles", "traffic.json"),
+                "sources": ("kernels_qlinear.hip", "device_common.h", "kernels.h"),
+                "kernels": ("k_qgemv", "k_qgemm_mfma")},
+    "tree": {"json": os.path.join(ROOT, "profiles", "traffic_tree.json"),
+             "sources": ("kernels_tree.hip", "device_common.h", "kernels.h"),
+             "kernels": ("k_tree_expand",)},
+}
 
 
 def parse():
@@ -73,9 +86,9 @@ def parse():
 
 # --- kernel identity and measured traffic ----------------------------------------
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(family: str = "qlinear") -> str:
     h = hashlib.sha256()
-    for f in ("kernels_qlinear.hip", "device_common.h", "kernels.h"):
+    for f in FAMILIES[family]["sources"]:
         with open(os.path.join(ROOT, "paper_2509_18344_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -115,9 +128,12 @@ def _counter_rows(d, counter):
     return [(meta[k][0], meta[k][1], meta[k][2], v) for k, v in per.items()]
 
 
-def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, calib_bytes=1 << 30):
-    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the qlinear kernels, scaled by
-    what the same counters read for a plain copy of known size."""
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family="qlinear",
+                  calib_bytes=1 << 30):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of one kernel family, scaled by what
+    the same counters read for a plain copy of known size."""
+    fam = FAMILIES[family]
+    pat = re.compile(r"(" + "|".join(fam["kernels"]) + r")<([^>]*)>")
     cf = max(v for (_, _, _, v) in _counter_rows(copy_fetch_dir, "FETCH_SIZE"))
     cw = max(v for (_, _, _, v) in _counter_rows(copy_write_dir, "WRITE_SIZE"))
     f_scale = calib_bytes / (cf * 1024.0)
@@ -125,11 +141,14 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, calib_by
     acc = collections.defaultdict(lambda: {"fetch": [], "write": [], "names": set()})
     for d, which, counter in ((fetch_dir, "fetch", "FETCH_SIZE"), (write_dir, "write", "WRITE_SIZE")):
         for name, grid, wg, v in _counter_rows(d, counter):
-            m = re.search(r"(k_qgemv|k_qgemm_mfma)<([^>]*)>", name)
+            m = pat.search(name)
             if not m:
                 continue
             targs = [int(a) for a in m.group(2).split(",")]
-            e = acc[dispatch_key(m.group(1), targs, grid, wg)]
+            if family == "qlinear":
+                e = acc[dispatch_key(m.group(1), targs, grid, wg)]
+            else:
+                e = acc[f"{m.group(0)} grid={grid} wg={wg}"]
             e[which].append(v)
             e["names"].add(m.group(0))
     kernels = {}
@@ -143,15 +162,15 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, calib_by
         kernels[key] = {"kernel": e["names"].pop(), "dispatches": len(e["fetch"]),
                         "fetch_kib_raw": round(fk, 1), "write_kib_raw": round(wk, 1),
                         "hbm_bytes_per_launch": int(round(fk * 1024 * f_scale + wk * 1024 * w_scale))}
-    out = {"kernel_source_sha256_16": kernel_source_hash(),
+    out = {"kernel_source_sha256_16": kernel_source_hash(family),
            "calibration": {"copy_bytes": calib_bytes, "fetch_kib_raw": cf, "write_kib_raw": cw,
                            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
            "kernels": kernels}
-    os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
-    with open(TRAFFIC_JSON, "w") as f:
+    os.makedirs(os.path.dirname(fam["json"]), exist_ok=True)
+    with open(fam["json"], "w") as f:
         json.dump(out, f, indent=1, sort_keys=True)
         f.write("\n")
-    print(json.dumps({"wrote": TRAFFIC_JSON, "kernels": len(kernels),
+    print(json.dumps({"wrote": fam["json"], "kernels": len(kernels),
                       "fetch_scale": out["calibration"]["fetch_scale"],
                       "write_scale": out["calibration"]["write_scale"]}))
 
@@ -184,15 +203,15 @@ def summarize_trace(d):
         print(f"| `{key}` | {len(a)} | {a.mean():.2f} | {np.median(a):.2f} | {a.min():.2f} | {a.max():.2f} |")
 
 
-def measured_traffic(key: str):
-    """HBM bytes per launch for `key` from profiles/traffic.json, if those counters
-    were taken on the current kernel sources; else None."""
+def measured_traffic(key: str, family: str = "qlinear"):
+    """HBM bytes per launch for `key` from the family's traffic file, if those
+    counters were taken on the current kernel sources; else None."""
     try:
-        with open(TRAFFIC_JSON) as f:
+        with open(FAMILIES[family]["json"]) as f:
             data = json.load(f)
     except (OSError, ValueError):
         return None
-    if data.get("kernel_source_sha256_16") != kernel_source_hash():
+    if data.get("kernel_source_sha256_16") != kernel_source_hash(family):
         return None
     entry = data.get("kernels", {}).get(key)
     return None if entry is None else entry.get("hbm_bytes_per_launch")
@@ -429,7 +448,7 @@ def run_stack(args, torch, ss, wl, ms, stream):
 def main():
     args = parse()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc)
+        summarize_pmc(*args.summarize_pmc, family="tree" if args.workload == "tree_expand" else "qlinear")
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
@@ -582,23 +601,26 @@ def run_tree(args, torch, ss):
 
     with torch.cuda.stream(stream):
         total_ms = timed(torch, stream, step, args.warmup, args.steps)
+        # Per R: a burst of back-to-back launches between two events on the launch
+        # stream (one event pair per launch would add the events' own cost).
         per_launch = []
         for (R, lg, parent, out) in sets:
-            ev = []
-            for r in range(max(args.per_launch_reps, len(lg))):
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
+            reps = max(args.per_launch_reps, len(lg))
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for r in range(reps):
                 call(R, lg, parent, out, r)
-                e1.record(stream)
-                ev.append((e0, e1))
+            e1.record(stream)
             torch.cuda.synchronize()
-            t = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3
+            avg_us = e0.elapsed_time(e1) * 1e3 / reps
             nbytes = 2 * R * TREE_V + 4 * R + 12 * TREE_K
-            per_launch.append({"R": R, "V": TREE_V, "k": TREE_K, "avg_us": round(float(t.mean()), 2),
-                               "p10_us": round(float(np.percentile(t, 10)), 2),
+            chunks, _, list_len = ss.subspec_tree_plan(R, TREE_V, TREE_K)
+            key = f"k_tree_expand<{list_len}> grid={R * chunks * 256} wg=256"
+            per_launch.append({"R": R, "V": TREE_V, "k": TREE_K, "key": key,
+                               "avg_us": round(avg_us, 2), "launches_timed": reps,
                                "alg_bytes": nbytes,
-                               "alg_GBs": round(nbytes / (t.mean() * 1e-6) / 1e9, 1)})
+                               "alg_GBs": round(nbytes / (avg_us * 1e-6) / 1e9, 1)})
     ms_per_step = total_ms / args.steps
     step_bytes = sum(2 * R * TREE_V for R in rs)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
@@ -614,8 +636,9 @@ def run_tree(args, torch, ss):
                    "rows": list(rs), "launches_per_step": len(rs), "timing": "eager launches"},
         "roofline": {"bound": "hbm", "achieved": dom["alg_GBs"], "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(dom["alg_GBs"] / HBM_PEAK_GBS, 4),
-                     "traffic": None, "kernel": f"k_tree_expand (R={dom['R']})",
-                     "avg_us": dom["avg_us"], "alg_bytes_per_launch": dom["alg_bytes"]},
+                     "traffic": measured_traffic(dom["key"], "tree"), "kernel": dom["key"],
+                     "avg_us": dom["avg_us"], "alg_bytes_per_launch": dom["alg_bytes"],
+                     "kernel_source_sha256_16": kernel_source_hash("tree")},
         "per_launch": per_launch,
     }
     if not args.no_cpu_baseline:

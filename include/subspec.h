@@ -219,6 +219,15 @@ int subspec_tree_expand(const void* logits, const float* parent_logp, int R, int
 /* Workspace bytes subspec_tree_expand needs for (R, V, k); 0 on bad arguments. */
 size_t subspec_tree_workspace_bytes(int R, int V, int k);
 
+/* Launch shape subspec_tree_expand uses for (R, V, k), computed on the host with no
+ * device access: every row is cut into `chunks` slices of `chunk_len` logits (the
+ * last may be shorter), one 256-thread workgroup each, so the grid has R * chunks
+ * workgroups; `list_len` is the per-thread candidate list length (8, 16 or 32, the
+ * kernel's template argument).  Outputs are host pointers.  Returns SUBSPEC_OK,
+ * SUBSPEC_EINVAL for a null output, or SUBSPEC_EUNSUPPORTED for an (R, V, k) that
+ * subspec_tree_expand would reject. */
+int subspec_tree_plan(int R, int V, int k, int* chunks, int* chunk_len, int* list_len);
+
 /* Grow the calling device's workspace to at least `bytes` now (synchronous, may
  * call hipMalloc), so that later calls, e.g. under stream capture, need not. */
 int subspec_reserve(size_t bytes);

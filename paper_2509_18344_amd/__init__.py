@@ -28,5 +28,6 @@ from ._binding import (  # noqa: F401
     subspec_graph_launch,
     subspec_graph_destroy,
     subspec_tree_expand,
+    subspec_tree_plan,
     subspec_tree_workspace_bytes,
 )

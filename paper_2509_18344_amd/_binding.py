@@ -73,6 +73,7 @@ def load_library():
         "subspec_graph_destroy": (I, [P]),
         "subspec_tree_expand": (I, [P, P, I, I, ctypes.c_float, I, P, P, P, P]),
         "subspec_tree_workspace_bytes": (S, [I, I, I]),
+        "subspec_tree_plan": (I, [I, I, I, P, P, P]),
         "subspec_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -207,3 +208,11 @@ def subspec_tree_expand(logits, parent_logp, R, V, temperature, k, parent_out, t
 
 def subspec_tree_workspace_bytes(R, V, k) -> int:
     return int(load_library().subspec_tree_workspace_bytes(R, V, k))
+
+
+def subspec_tree_plan(R, V, k):
+    """(chunks, chunk_len, list_len) of the expansion launch for (R, V, k)."""
+    c, n, l = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check("subspec_tree_plan", load_library().subspec_tree_plan(
+        R, V, k, ctypes.byref(c), ctypes.byref(n), ctypes.byref(l)))
+    return c.value, n.value, l.value

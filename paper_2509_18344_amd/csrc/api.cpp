@@ -588,6 +588,16 @@ size_t subspec_tree_workspace_bytes(int R, int V, int k) {
   return subspec::tree_workspace_bytes(R, V, k);
 }
 
+int subspec_tree_plan(int R, int V, int k, int* chunks, int* chunk_len, int* list_len) {
+  if (!chunks || !chunk_len || !list_len) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (R < 1 || R > subspec::kTreeMaxRows || V < 8 || V % 8 || k < 1 || k > subspec::kTreeMaxK ||
+      static_cast<long long>(R) * V >= (1LL << 31) || k > static_cast<long long>(R) * V)
+    return fail(SUBSPEC_EUNSUPPORTED, "tree_plan: (R, V, k) out of the supported range");
+  subspec::tree_plan(R, V, chunks, chunk_len);
+  *list_len = k <= 8 ? 8 : k <= 16 ? 16 : 32;
+  return SUBSPEC_OK;
+}
+
 int subspec_tree_expand(const void* logits, const float* parent_logp, int R, int V,
                         float temperature, int k, int* parent_out, int* token_out,
                         float* score_out, hipStream_t stream) {

@@ -161,3 +161,20 @@ def test_tree_expand_argument_errors_need_no_gpu():
         ss.subspec_tree_expand(24, 16, 2, 64, 0.2, 4, 16, 16, 16, stream=0)
     assert ss.subspec_tree_workspace_bytes(6, 152064, 6) > 65536
     assert ss.subspec_tree_workspace_bytes(6, 100, 6) == 0
+
+
+def test_tree_plan_shapes():
+    # about 512 workgroups, each at least 2048 logits (one 16-byte load per thread)
+    # unless the row is shorter; slices are multiples of 8 and cover the row
+    assert ss.subspec_tree_plan(6, 152064, 6) == (75, 2032, 8)
+    assert ss.subspec_tree_plan(64, 152064, 6) == (8, 19008, 8)
+    assert ss.subspec_tree_plan(1, 152064, 6) == (75, 2032, 8)
+    assert ss.subspec_tree_plan(1024, 64, 32) == (1, 64, 32)
+    assert ss.subspec_tree_plan(37, 4096, 17) == (2, 2048, 32)
+    assert ss.subspec_tree_plan(3, 2048, 9)[2] == 16
+    for R, V, k in [(1, 8, 1), (6, 1000, 6), (128, 152064, 6), (1000, 2048, 32), (7, 152064, 16)]:
+        c, n, _ = ss.subspec_tree_plan(R, V, k)
+        assert n % 8 == 0 and (c - 1) * n < V <= c * n and R * c <= 1024, (R, V, k)
+    for R, V, k in [(0, 64, 1), (2, 100, 1), (2, 64, 33), (1, 8, 9)]:
+        with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
+            ss.subspec_tree_plan(R, V, k)
