@@ -52,7 +52,7 @@ FAMILIES = {
                 "sources": ("kernels_qlinear.hip", "device_common.h", "kernels.h"),
                 "kernels": ("k_qgemv", "k_qgemm_mfma")},
     "tree": {"json": os.path.join(ROOT, "profiles", "traffic_tree.json"),
-             "sources": ("kernels_tree.hip", "device_common.h", "kernels.h"),
+             "sources": ("kernels_tree.hip", "kernels_tree.h", "device_common.h", "kernels.h"),
              "kernels": ("k_tree_expand",)},
 }
 

@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "kernels_tree.h"
 
 namespace {
 

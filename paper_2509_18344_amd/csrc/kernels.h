@@ -59,28 +59,6 @@ hipError_t launch_qpack(const uint8_t* codes, int bits, int N, int K, void* qw, 
 hipError_t launch_qdequant(const void* qw, const void* sc, const void* zr, int bits, int group,
                            int N, int K, float* wf, uint16_t* wb, hipStream_t st);
 
-// Draft-tree expansion (kernels_tree.hip): logits bf16 [R][V], path scores fp32 [R].
-constexpr int kTreeMaxRows = 1024;
-constexpr int kTreeMaxK = 32;
-struct TreeArgs {
-  const uint16_t* logits;
-  const float* parent;
-  int R, V, k;
-  float inv_t;            // 1 / temperature
-  int chunks, chunk_len;  // workgroups per row and the logits each one covers
-  float* stat_m;          // [R * chunks] running maxima
-  float* stat_s;          // [R * chunks] sums of exp(z - m)
-  float* cand_val;        // [R * chunks][k] best z of each workgroup
-  int* cand_idx;          // [R * chunks][k] their tokens
-  unsigned* cnt;          // completion counter (zero between launches)
-  int* out_parent;
-  int* out_token;
-  float* out_score;
-};
-void tree_plan(int R, int V, int* chunks, int* chunk_len);
-size_t tree_workspace_bytes(int R, int V, int k);
-hipError_t launch_tree_expand(const TreeArgs& a, hipStream_t st);
-
 // Split-K workspace: kSplitCounters zeroed counters, then the fp32 partial sums.
 constexpr int kSplitCounters = 16384;
 constexpr size_t kSplitCounterBytes = kSplitCounters * sizeof(unsigned);

@@ -17,7 +17,7 @@
 #include <cmath>
 
 #include "device_common.h"
-#include "kernels.h"
+#include "kernels_tree.h"
 
 namespace subspec {
 
