@@ -1,5 +1,6 @@
 """Plain fp64 CPU oracle for the low-bit substitute-layer linear (SubSpec, Sec. 4.1)
-and for the draft-tree expansion step with probability sharpening (Sec. 4.2, App. D).
+and for the draft-tree expansion step with probability sharpening (Sec. 4.2, App. D)
+and the draft model's tree attention over the shared KV cache (Sec. 4.1).
 
 TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import or call anything in this package.
@@ -27,4 +28,9 @@ from .tree import (  # noqa: F401
     expand_scores,
     tree_expand,
     kth_gap,
+)
+from .tree_attn import (  # noqa: F401
+    append_kv,
+    tree_attention,
+    weighted_abs_v,
 )

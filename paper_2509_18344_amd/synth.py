@@ -64,3 +64,45 @@ def layer_weights(projs, cfg: int, layer: int, device="cuda"):
     from its own seeded stream (cfg, layer, projection index)."""
     return {p.name: weights_torch(p.N, p.K, cfg, layer, i, device=device)
             for i, p in enumerate(projs)}
+
+
+def tree_levels_mask(T: int, k: int, M: int, *keys: int) -> np.ndarray:
+    """Ancestor mask of a random draft tree, as uint32 bit rows [M][ceil((T + M) / 32)].
+
+    The T tree tokens already in the cache come in levels of k in cache order (the
+    last level may be shorter); each token's parent is a uniformly chosen token of
+    the level before, the first level hanging off the prefix.  The M new tokens form
+    the next level.  Bit j of row i is set when tree token j (cache position
+    prefix + j) is an ancestor of new token i, and bit T + i marks the token itself.
+    """
+    rng = np.random.default_rng(np.random.SeedSequence([int(x) for x in keys] + [11]))
+    parent = np.full(T + M, -1, dtype=np.int64)
+    levels = [list(range(s, min(s + k, T))) for s in range(0, T, k)]
+    for lv in range(1, len(levels)):
+        for j in levels[lv]:
+            parent[j] = rng.choice(levels[lv - 1])
+    for i in range(M):
+        parent[T + i] = rng.choice(levels[-1]) if levels else -1
+    W = (T + M + 31) // 32
+    mask = np.zeros((M, W), dtype=np.uint32)
+    for i in range(M):
+        j = T + i
+        while j >= 0:
+            mask[i, j // 32] |= np.uint32(1 << (j % 32))
+            j = parent[j]
+    return mask
+
+
+def tree_attn_inputs(M: int, Hq: int, Hkv: int, D: int, S: int, *keys: int, q_scale: float = 1.0):
+    """bf16 bit patterns (uint16) of one layer's tree-attention inputs: q [M][Hq][D]
+    (N(0, q_scale^2)), K and V caches [Hkv][S][D], new keys and values [M][Hkv][D]
+    (all N(0, 1)); float32 draws rounded to bf16 (round to nearest even)."""
+    import torch
+    rng = np.random.default_rng(np.random.SeedSequence([int(x) for x in keys] + [13]))
+
+    def bf(shape, s=1.0):
+        a = rng.standard_normal(shape, dtype=np.float32) * np.float32(s)
+        return bf16_bits(torch.from_numpy(a).to(torch.bfloat16))
+
+    return {"q": bf((M, Hq, D), q_scale), "k_cache": bf((Hkv, S, D)), "v_cache": bf((Hkv, S, D)),
+            "k_new": bf((M, Hkv, D)), "v_new": bf((M, Hkv, D))}
