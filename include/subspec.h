@@ -228,6 +228,46 @@ size_t subspec_tree_workspace_bytes(int R, int V, int k);
  * subspec_tree_expand would reject. */
 int subspec_tree_plan(int R, int V, int k, int* chunks, int* chunk_len, int* list_len);
 
+/* Tree attention of one decoder layer in one draft pass, over the key/value cache the
+ * draft model shares with the target (SubSpec Sec. 4.1, "Shared KV-Cache"; the tree
+ * masks of tree decoding, Sec. 2 and Sec. 4.2).  M new tree tokens with Hq query
+ * heads (head dimension 128) grouped onto Hkv key/value heads (query head h reads
+ * key/value head h / (Hq / Hkv)) attend, with scores q.k * scale and a softmax, to
+ *   - every committed cache position 0 .. P - 1,
+ *   - cache position P + j (j < T: tree tokens of earlier passes; j = T + i: new
+ *     token i) when bit j of their mask row is set.
+ * The new keys and values are appended to the cache at P + T .. P + T + M - 1 (the
+ * target's verification later overwrites them); within this call the new tokens'
+ * keys and values are read from k_new / v_new.  A query with no visible position
+ * gets zeros.
+ *   q        device bf16 [M][Hq][128] (positions already rotated)
+ *   k_cache  device bf16 [Hkv][S][128], one layer; rows P + T .. P + T + M - 1 are
+ *   v_cache  overwritten with k_new / v_new, all others are only read
+ *   k_new    device bf16 [M][Hkv][128]
+ *   v_new    device bf16 [M][Hkv][128]
+ *   mask     device uint32 [M][W], W = ceil((T + M) / 32); bit j % 32 of word j / 32
+ *            of row i allows tree position j to token i
+ *   out      device bf16 [M][Hq][128]
+ * Needs Hkv >= 1, Hq a multiple of Hkv, 1 <= M and (Hq / Hkv) * M <= 64, P, T >= 0,
+ * P + T + M <= S, M * W <= 2048, a finite scale; q, caches, new rows and out 16-byte
+ * aligned, mask 4-byte aligned; out must not overlap the inputs.  Two kernels on
+ * `stream` (partial outputs per key range, then their combination and the append);
+ * workspace as for subspec_qlinear (subspec_tree_attention_workspace_bytes). */
+int subspec_tree_attention(const void* q, void* k_cache, void* v_cache, const void* k_new,
+                           const void* v_new, const uint32_t* mask, int M, int Hq, int Hkv,
+                           int S, int P, int T, float scale, void* out, hipStream_t stream);
+
+/* Workspace bytes subspec_tree_attention needs; 0 on bad arguments. */
+size_t subspec_tree_attention_workspace_bytes(int M, int Hq, int Hkv, int P, int T);
+
+/* Launch shape of subspec_tree_attention, on the host: the P + T + M keys of each
+ * key/value head are cut into `splits` ranges of `tiles_per_split` tiles of 32 keys;
+ * the first kernel runs splits x Hkv workgroups.  Returns SUBSPEC_OK, SUBSPEC_EINVAL
+ * for a null output or SUBSPEC_EUNSUPPORTED for shapes subspec_tree_attention would
+ * reject (S is not checked here). */
+int subspec_tree_attention_plan(int M, int Hq, int Hkv, int P, int T, int* splits,
+                                int* tiles_per_split);
+
 /* Grow the calling device's workspace to at least `bytes` now (synchronous, may
  * call hipMalloc), so that later calls, e.g. under stream capture, need not. */
 int subspec_reserve(size_t bytes);

@@ -28,6 +28,9 @@ from ._binding import (  # noqa: F401
     subspec_graph_launch,
     subspec_graph_destroy,
     subspec_tree_expand,
+    subspec_tree_attention,
+    subspec_tree_attention_plan,
+    subspec_tree_attention_workspace_bytes,
     subspec_tree_plan,
     subspec_tree_workspace_bytes,
 )

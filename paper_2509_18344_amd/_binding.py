@@ -74,6 +74,9 @@ def load_library():
         "subspec_tree_expand": (I, [P, P, I, I, ctypes.c_float, I, P, P, P, P]),
         "subspec_tree_workspace_bytes": (S, [I, I, I]),
         "subspec_tree_plan": (I, [I, I, I, P, P, P]),
+        "subspec_tree_attention": (I, [P, P, P, P, P, P, I, I, I, I, I, I, ctypes.c_float, P, P]),
+        "subspec_tree_attention_workspace_bytes": (S, [I, I, I, I, I]),
+        "subspec_tree_attention_plan": (I, [I, I, I, I, I, P, P]),
         "subspec_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -208,6 +211,25 @@ def subspec_tree_expand(logits, parent_logp, R, V, temperature, k, parent_out, t
 
 def subspec_tree_workspace_bytes(R, V, k) -> int:
     return int(load_library().subspec_tree_workspace_bytes(R, V, k))
+
+
+def subspec_tree_attention(q, k_cache, v_cache, k_new, v_new, mask, M, Hq, Hkv, S, P, T, scale, out,
+                           stream=None):
+    return _check("subspec_tree_attention", load_library().subspec_tree_attention(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_new), _ptr(v_new), _ptr(mask), M, Hq, Hkv, S, P, T,
+        scale, _ptr(out), _stream(stream)))
+
+
+def subspec_tree_attention_workspace_bytes(M, Hq, Hkv, P, T) -> int:
+    return int(load_library().subspec_tree_attention_workspace_bytes(M, Hq, Hkv, P, T))
+
+
+def subspec_tree_attention_plan(M, Hq, Hkv, P, T):
+    """(splits, tiles_per_split) of the tree-attention launch."""
+    s, t = ctypes.c_int(), ctypes.c_int()
+    _check("subspec_tree_attention_plan", load_library().subspec_tree_attention_plan(
+        M, Hq, Hkv, P, T, ctypes.byref(s), ctypes.byref(t)))
+    return s.value, t.value
 
 
 def subspec_tree_plan(R, V, k):

@@ -9,7 +9,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsubspec.so")
 HOST_SOURCES = ["api.cpp"]
-DEVICE_SOURCES = ["kernels_qlinear.hip", "kernels_prep.hip", "kernels_tree.hip"]
+DEVICE_SOURCES = ["kernels_qlinear.hip", "kernels_prep.hip", "kernels_tree.hip", "kernels_attn.hip"]
 OBJDIR = os.path.join(ROOT, "_build")
 
 HIPCC_FLAGS = [

@@ -16,6 +16,7 @@
 
 #include "kernels.h"
 #include "kernels_tree.h"
+#include "kernels_attn.h"
 
 namespace {
 
@@ -587,6 +588,78 @@ size_t subspec_tree_workspace_bytes(int R, int V, int k) {
   if (R < 1 || R > subspec::kTreeMaxRows || V < 8 || V % 8 || k < 1 || k > subspec::kTreeMaxK)
     return 0;
   return subspec::tree_workspace_bytes(R, V, k);
+}
+
+namespace {
+
+// Shape checks shared by the tree-attention entry points ("" when supported).
+const char* attn_shape_error(int M, int Hq, int Hkv, int P, int T) {
+  if (Hkv < 1 || Hq < Hkv || Hq % Hkv) return "Hq must be a positive multiple of Hkv";
+  if (M < 1 || static_cast<long long>(Hq / Hkv) * M > subspec::kAttnMaxRows)
+    return "need 1 <= M and (Hq / Hkv) * M <= 64";
+  if (P < 0 || T < 0 || static_cast<long long>(P) + T + M >= (1ll << 30)) return "P, T out of range";
+  const long long W = (static_cast<long long>(T) + M + 31) / 32;
+  if (M * W > subspec::kAttnMaskWords) return "M * ceil((T + M) / 32) must be at most 2048";
+  return "";
+}
+
+}  // namespace
+
+int subspec_tree_attention_plan(int M, int Hq, int Hkv, int P, int T, int* splits, int* tiles_per_split) {
+  if (!splits || !tiles_per_split) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  const char* why = attn_shape_error(M, Hq, Hkv, P, T);
+  if (*why) return fail(SUBSPEC_EUNSUPPORTED, "tree_attention: %s", why);
+  subspec::attn_plan(M, Hq, Hkv, P, T, splits, tiles_per_split);
+  return SUBSPEC_OK;
+}
+
+size_t subspec_tree_attention_workspace_bytes(int M, int Hq, int Hkv, int P, int T) {
+  if (*attn_shape_error(M, Hq, Hkv, P, T)) return 0;
+  return subspec::attn_workspace_bytes(M, Hq, Hkv, P, T);
+}
+
+int subspec_tree_attention(const void* q, void* k_cache, void* v_cache, const void* k_new,
+                           const void* v_new, const uint32_t* mask, int M, int Hq, int Hkv,
+                           int S, int P, int T, float scale, void* out, hipStream_t stream) {
+  if (!q || !k_cache || !v_cache || !k_new || !v_new || !mask || !out)
+    return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_new) ||
+      !aligned16(v_new) || !aligned16(out))
+    return fail(SUBSPEC_EINVAL, "q, caches, new keys/values and out must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(mask) & 3u) return fail(SUBSPEC_EINVAL, "mask must be 4-byte aligned");
+  const char* why = attn_shape_error(M, Hq, Hkv, P, T);
+  if (*why) return fail(SUBSPEC_EUNSUPPORTED, "tree_attention: %s", why);
+  if (static_cast<long long>(P) + T + M > S)
+    return fail(SUBSPEC_EUNSUPPORTED, "tree_attention: P + T + M = %lld exceeds S = %d",
+                static_cast<long long>(P) + T + M, S);
+  if (!std::isfinite(scale)) return fail(SUBSPEC_EINVAL, "scale must be finite");
+  void* ws = nullptr;
+  const int rc = get_workspace(subspec::attn_workspace_bytes(M, Hq, Hkv, P, T), stream, &ws);
+  if (rc) return rc;
+  subspec::AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_cache = static_cast<uint16_t*>(k_cache);
+  a.v_cache = static_cast<uint16_t*>(v_cache);
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.mask = mask;
+  a.M = M;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.S = S;
+  a.P = P;
+  a.T = T;
+  a.W = (T + M + 31) / 32;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  subspec::attn_plan(M, Hq, Hkv, P, T, &a.splits, &a.tiles_per_split);
+  a.rows_pad = 16 * ((Hq / Hkv * M + 15) / 16);
+  const size_t n = static_cast<size_t>(Hkv) * a.splits * a.rows_pad;
+  a.part_o = static_cast<float*>(ws);
+  a.part_ml = a.part_o + n * subspec::kAttnD;
+  a.out = static_cast<uint16_t*>(out);
+  const hipError_t e = subspec::launch_tree_attention(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "tree_attention launch");
+  return SUBSPEC_OK;
 }
 
 int subspec_tree_plan(int R, int V, int k, int* chunks, int* chunk_len, int* list_len) {

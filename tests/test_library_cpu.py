@@ -178,3 +178,36 @@ def test_tree_plan_shapes():
     for R, V, k in [(0, 64, 1), (2, 100, 1), (2, 64, 33), (1, 8, 9)]:
         with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
             ss.subspec_tree_plan(R, V, k)
+
+
+def test_tree_attention_plan_and_errors_need_no_gpu():
+    # Qwen2.5-7B at the last pass of a depth-48 tree: 2336 keys = 73 tiles of 32,
+    # two tiles per range
+    assert ss.subspec_tree_attention_plan(6, 28, 4, 2048, 282) == (37, 2)
+    for M, Hq, Hkv, P, T in [(6, 28, 4, 0, 0), (1, 1, 1, 0, 0), (6, 40, 8, 30000, 282), (8, 16, 2, 33, 7)]:
+        s, t = ss.subspec_tree_attention_plan(M, Hq, Hkv, P, T)
+        tiles = -(-(P + T + M) // 32)
+        assert t >= 1 and (s - 1) * t < tiles <= s * t, (M, Hq, Hkv, P, T)
+        rows_pad = 16 * -(-(Hq // Hkv * M) // 16)
+        assert ss.subspec_tree_attention_workspace_bytes(M, Hq, Hkv, P, T) == Hkv * s * rows_pad * (128 + 2) * 4
+    for M, Hq, Hkv, P, T in [(6, 30, 4, 10, 0), (0, 28, 4, 10, 0), (10, 28, 4, 10, 0), (6, 28, 4, -1, 0),
+                             (64, 1, 1, 0, 1100), (6, 4, 0, 10, 0)]:
+        with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
+            ss.subspec_tree_attention_plan(M, Hq, Hkv, P, T)
+        assert ss.subspec_tree_attention_workspace_bytes(M, Hq, Hkv, P, T) == 0
+    args = dict(M=6, Hq=28, Hkv=4, S=2400, P=2048, T=282, scale=0.088)
+
+    def call(q=16, kc=16, vc=16, kn=16, vn=16, mask=16, out=16, **kw):
+        a = dict(args, **kw)
+        return ss.subspec_tree_attention(q, kc, vc, kn, vn, mask, a["M"], a["Hq"], a["Hkv"], a["S"], a["P"],
+                                         a["T"], a["scale"], out, stream=0)
+    with pytest.raises(ss.SubspecError, match="EINVAL"):
+        call(q=None)
+    with pytest.raises(ss.SubspecError, match="EINVAL"):
+        call(kc=24)
+    with pytest.raises(ss.SubspecError, match="EINVAL"):
+        call(mask=18)
+    with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
+        call(S=2335)
+    with pytest.raises(ss.SubspecError, match="EINVAL"):
+        call(scale=float("inf"))
