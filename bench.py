@@ -25,7 +25,11 @@ tree_expand``: profiles/traffic_tree.json), which later runs read for
 ``roofline.traffic`` while that kernel family's sources are unchanged.
 
 ``--workload tree_expand`` times the draft-tree expansion step instead (sharpened
-log-softmax of R x 152064 bf16 logits, parent scores, global top-6).
+log-softmax of R x 152064 bf16 logits, parent scores, global top-6), and
+``--workload tree_attn`` one layer's tree attention over the shared KV cache
+(Qwen2.5-7B heads, 6 new tree tokens, 2048 committed positions, 282 earlier tree
+tokens: the last pass of a depth-48 tree).  Their traffic files are
+profiles/traffic_tree.json and profiles/traffic_attn.json.
 """
 from __future__ import annotations
 
@@ -54,7 +58,11 @@ FAMILIES = {
     "tree": {"json": os.path.join(ROOT, "profiles", "traffic_tree.json"),
              "sources": ("kernels_tree.hip", "kernels_tree.h", "device_common.h", "kernels.h"),
              "kernels": ("k_tree_expand",)},
+    "attn": {"json": os.path.join(ROOT, "profiles", "traffic_attn.json"),
+             "sources": ("kernels_attn.hip", "kernels_attn.h", "device_common.h", "kernels.h"),
+             "kernels": ("k_attn_partial", "k_attn_combine")},
 }
+WORKLOAD_FAMILY = {"tree_expand": "tree", "tree_attn": "attn"}
 
 
 def parse():
@@ -64,7 +72,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen7b_mlp",
                     help="qwen7b_mlp (default), qwen7b_stack, qwen32b_stack, qwen32b_2bit, tiny, "
-                         "or tree_expand (the draft-tree expansion step; --ms gives its rows)")
+                         "or tree_expand (the draft-tree expansion step; --ms gives its rows) "
+                         "or tree_attn (one layer's tree attention over the shared KV cache)")
     ap.add_argument("--ms", default=None, help="comma-separated M values (default: the workload's)")
     ap.add_argument("--rotate-gb", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -133,7 +142,7 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family="
     """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of one kernel family, scaled by what
     the same counters read for a plain copy of known size."""
     fam = FAMILIES[family]
-    pat = re.compile(r"(" + "|".join(fam["kernels"]) + r")<([^>]*)>")
+    pat = re.compile(r"(" + "|".join(fam["kernels"]) + r")(<([^>]*)>)?")
     cf = max(v for (_, _, _, v) in _counter_rows(copy_fetch_dir, "FETCH_SIZE"))
     cw = max(v for (_, _, _, v) in _counter_rows(copy_write_dir, "WRITE_SIZE"))
     f_scale = calib_bytes / (cf * 1024.0)
@@ -144,7 +153,7 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family="
             m = pat.search(name)
             if not m:
                 continue
-            targs = [int(a) for a in m.group(2).split(",")]
+            targs = [int(a) for a in m.group(3).split(",")] if m.group(3) else []
             if family == "qlinear":
                 e = acc[dispatch_key(m.group(1), targs, grid, wg)]
             else:
@@ -448,7 +457,7 @@ def run_stack(args, torch, ss, wl, ms, stream):
 def main():
     args = parse()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, family="tree" if args.workload == "tree_expand" else "qlinear")
+        summarize_pmc(*args.summarize_pmc, family=WORKLOAD_FAMILY.get(args.workload, "qlinear"))
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
@@ -476,6 +485,9 @@ def main():
     ss.load_library()
     if args.workload == "tree_expand":
         run_tree(args, torch, ss)
+        return
+    if args.workload == "tree_attn":
+        run_attn(args, torch, ss)
         return
     wl = WORKLOADS[args.workload]
     ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else wl.ms
@@ -644,6 +656,115 @@ def run_tree(args, torch, ss):
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = tree_cpu_baseline(rs)
     line = json.dumps(out)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(line + "\n")
+    print(line, flush=True)
+
+
+
+
+# One draft layer's tree attention, Qwen2.5-7B heads, at the last pass of a depth-48
+# tree with k = 6 (Sec. 5.1): 47 earlier passes x 6 tokens = 282 tree tokens.
+ATTN_CFG = {"M": 6, "Hq": 28, "Hkv": 4, "P": 2048, "T": 282}
+
+
+def attn_bytes(M, Hq, Hkv, P, T):
+    """Algorithmic bytes of one call: every visible-or-not key and value row of the
+    head's range read once (bf16), q and the output, the appended rows, the mask."""
+    L = P + T + M
+    W = (T + M + 31) // 32
+    return 2 * Hkv * L * 128 * 2 + 2 * M * Hq * 128 * 2 + 2 * M * Hkv * 128 * 2 + 4 * M * W
+
+
+def attn_cpu_baseline(min_seconds=10.0):
+    """Time the fp64 oracle on the bench configuration until `min_seconds` pass."""
+    import oracle
+    from paper_2509_18344_amd import synth
+    c = ATTN_CFG
+    S = c["P"] + c["T"] + c["M"]
+    x = synth.tree_attn_inputs(c["M"], c["Hq"], c["Hkv"], 128, S, 5)
+    mask = synth.tree_levels_mask(c["T"], 6, c["M"], 5)
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.tree_attention(x["q"], x["k_cache"], x["v_cache"], c["P"], c["T"], x["k_new"], x["v_new"],
+                              mask, 1.0 / math.sqrt(128))
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    nbytes = steps * attn_bytes(**c)
+    return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "seconds": round(dt, 3),
+            "sample": f"{steps} call(s) of the tree attention at {c} (NumPy fp64, one thread)"}
+
+
+def run_attn(args, torch, ss):
+    """One step = one call (two kernels) on one layer's cache; the caches rotate over
+    >= --rotate-gb of distinct copies so that they come from HBM."""
+    from paper_2509_18344_amd import synth
+    c = ATTN_CFG
+    M, Hq, Hkv, P, T = c["M"], c["Hq"], c["Hkv"], c["P"], c["T"]
+    S = P + T + M
+    x = synth.tree_attn_inputs(M, Hq, Hkv, 128, S, 5)
+    mask = synth.tree_levels_mask(T, 6, M, 5)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to("cuda")
+    per = 2 * Hkv * S * 128 * 2
+    copies = max(2, int(math.ceil(args.rotate_gb * 1e9 / per)))
+    kc0, vc0 = dev(x["k_cache"]), dev(x["v_cache"])
+    caches = [(kc0.clone(), vc0.clone()) for _ in range(copies)]
+    q, kn, vn = dev(x["q"]), dev(x["k_new"]), dev(x["v_new"])
+    mk = torch.from_numpy(mask.view(np.int32)).to("cuda")
+    out = torch.empty((M, Hq, 128), dtype=torch.int16, device="cuda")
+    scale = 1.0 / math.sqrt(128)
+    ss.subspec_reserve(ss.subspec_tree_attention_workspace_bytes(M, Hq, Hkv, P, T))
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def step(s):
+        kc, vc = caches[s % copies]
+        ss.subspec_tree_attention(q, kc, vc, kn, vn, mk, M, Hq, Hkv, S, P, T, scale, out, stream)
+
+    with torch.cuda.stream(stream):
+        total_ms = timed(torch, stream, step, args.warmup, args.steps)
+        reps = max(args.per_launch_reps, copies)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for r in range(reps):
+            step(r)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        avg_us = e0.elapsed_time(e1) * 1e3 / reps
+    ms_per_step = total_ms / args.steps
+    nbytes = attn_bytes(**c)
+    splits, tps = ss.subspec_tree_attention_plan(M, Hq, Hkv, P, T)
+    qt = -(-(Hq // Hkv * M) // 16)
+    keys = [f"k_attn_partial<{qt}> grid={splits * 256} wg=256", f"k_attn_combine grid={M * Hq * 128} wg=128"]
+    tr = [measured_traffic(k, "attn") for k in keys]
+    achieved = nbytes / (avg_us * 1e-6) / 1e9
+    value = nbytes / (ms_per_step * 1e-3) / 1e9
+    out_line = {
+        "metric": "KV-cache GB/s of the draft model's tree attention (one layer, one draft pass)",
+        "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: N(0,1) bf16 q, keys, values; random depth-48 tree mask; seeded",
+        "config": {"workload": f"tree attention, Qwen2.5-7B heads (Hq=28, Hkv=4, D=128), M={M} new tree "
+                               f"tokens, P={P} committed, T={T} earlier tree tokens",
+                   "splits": splits, "tiles_per_split": tps, "cache_copies": copies,
+                   "timing": "eager calls (two kernels each)"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None if None in tr else sum(tr),
+                     "kernel": " + ".join(keys) + " (one call)", "avg_us": round(avg_us, 2),
+                     "calls_timed": reps, "alg_bytes_per_launch": nbytes,
+                     "kernel_source_sha256_16": kernel_source_hash("attn")},
+    }
+    if not args.no_cpu_baseline:
+        out_line["cpu_baseline"] = attn_cpu_baseline()
+    line = json.dumps(out_line)
     if args.json_out:
         with open(args.json_out, "w") as f:
             f.write(line + "\n")

@@ -652,6 +652,8 @@ int subspec_tree_attention(const void* q, void* k_cache, void* v_cache, const vo
   a.W = (T + M + 31) / 32;
   a.scale_log2 = scale * 1.4426950408889634f;
   subspec::attn_plan(M, Hq, Hkv, P, T, &a.splits, &a.tiles_per_split);
+  if (a.splits > subspec::kAttnMaxSplits)
+    return fail(SUBSPEC_EUNSUPPORTED, "tree_attention: %d key ranges exceed %d", a.splits, subspec::kAttnMaxSplits);
   a.rows_pad = 16 * ((Hq / Hkv * M + 15) / 16);
   const size_t n = static_cast<size_t>(Hkv) * a.splits * a.rows_pad;
   a.part_o = static_cast<float*>(ws);

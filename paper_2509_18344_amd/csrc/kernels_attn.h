@@ -10,6 +10,7 @@ constexpr int kAttnD = 128;           // head dimension (Qwen2.5 models)
 constexpr int kAttnTile = 32;         // keys per tile
 constexpr int kAttnMaxRows = 64;      // query rows per key/value head: (Hq / Hkv) * M
 constexpr int kAttnMaskWords = 2048;  // M * ceil((T + M) / 32)
+constexpr int kAttnMaxSplits = 512;   // key ranges per head (attn_plan gives at most 256)
 
 struct AttnArgs {
   const uint16_t* q;      // bf16 [M][Hq][D]

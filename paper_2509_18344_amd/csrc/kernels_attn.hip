@@ -236,26 +236,43 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_partial(AttnArgs a) {
   }
 }
 
-// One workgroup per (token i, query head h), one thread per dimension.
+// One workgroup per (token i, query head h), one thread per dimension.  Each range's
+// (max, sum) pair is read once into LDS and turned into a weight; the partial
+// outputs are then read in batches of independent loads and summed in range order.
 __global__ __launch_bounds__(kAttnD) void k_attn_combine(AttnArgs a) {
+  __shared__ float sm[kAttnMaxSplits], sl[kAttnMaxSplits];
+  constexpr int kBatch = 16;
   const int i = blockIdx.x / a.Hq, h = blockIdx.x % a.Hq;
   const int d = threadIdx.x;
   const int G = a.Hq / a.Hkv;
   const int g = h / G, hl = h % G;
   const int row = hl * a.M + i;
-  const size_t base = static_cast<size_t>(g) * a.splits * a.rows_pad + row;
+  const int ns = a.splits;
+  const size_t base = static_cast<size_t>(g) * ns * a.rows_pad + row;
+  for (int s = d; s < ns; s += kAttnD) {
+    const size_t b = base + static_cast<size_t>(s) * a.rows_pad;
+    sm[s] = a.part_ml[2 * b];
+    sl[s] = a.part_ml[2 * b + 1];
+  }
+  __syncthreads();
   float mmax = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) mmax = fmaxf(mmax, a.part_ml[2 * (base + static_cast<size_t>(s) * a.rows_pad)]);
-  float num = 0.f, den = 0.f;
-  if (mmax != -INFINITY)
-    for (int s = 0; s < a.splits; ++s) {
-      const size_t b = base + static_cast<size_t>(s) * a.rows_pad;
-      const float ms = a.part_ml[2 * b];
-      if (ms == -INFINITY) continue;
-      const float w = exp2f(ms - mmax);
-      den += w * a.part_ml[2 * b + 1];
-      num += w * a.part_o[b * kAttnD + d];
-    }
+  for (int s = 0; s < ns; ++s) mmax = fmaxf(mmax, sm[s]);
+  __syncthreads();
+  for (int s = d; s < ns; s += kAttnD) sm[s] = sm[s] == -INFINITY ? 0.f : exp2f(sm[s] - mmax);
+  __syncthreads();
+  float den = 0.f, num = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      v[u] = s0 + u < ns ? a.part_o[(base + static_cast<size_t>(s0 + u) * a.rows_pad) * kAttnD + d] : 0.f;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (s0 + u < ns) {
+        den += sm[s0 + u] * sl[s0 + u];
+        num += sm[s0 + u] * v[u];
+      }
+  }
   a.out[(static_cast<size_t>(i) * a.Hq + h) * kAttnD + d] = float_to_bf16_bits(den > 0.f ? num / den : 0.f);
   // append this token's key and value for head g (once per key/value head)
   if (hl == 0) {
