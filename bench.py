@@ -742,7 +742,9 @@ def run_attn(args, torch, ss):
     splits, tps = ss.subspec_tree_attention_plan(M, Hq, Hkv, P, T)
     qt = -(-(Hq // Hkv * M) // 16)
     keys = [f"k_attn_partial<{qt}> grid={splits * 256} wg=256", f"k_attn_combine grid={M * Hq * 128} wg=128"]
-    tr = [measured_traffic(k, "attn") for k in keys]
+    # the counter files give the whole 2-D grid (splits x Hkv workgroups)
+    tr = [measured_traffic(k, "attn") for k in
+          (f"k_attn_partial<{qt}> grid={splits * 256 * Hkv} wg=256", keys[1])]
     achieved = nbytes / (avg_us * 1e-6) / 1e9
     value = nbytes / (ms_per_step * 1e-3) / 1e9
     out_line = {

@@ -45,10 +45,30 @@ __device__ __forceinline__ int value_slot(int key) {
 }
 
 struct AttnLds {
-  uint16_t k[2][kAttnTile][kKRow];
-  uint16_t vt[2][kAttnD][kVRow];
-  uint32_t mask[kAttnMaskWords];
+  alignas(16) uint16_t k[2][kAttnTile][kKRow];
+  alignas(16) uint16_t vt[2][kAttnD][kVRow];
+  alignas(16) uint32_t mask[kAttnMaskWords];
 };
+
+// Visibility of the 32 keys key0 .. key0 + 31 for one query row (bit k: key0 + k):
+// committed positions (< P) always, tree positions P + j by bit j of the row's mask,
+// nothing at or past k_end.  `row_mask` is the row's W words in LDS.
+__device__ __forceinline__ uint32_t tile_visibility(const uint32_t* row_mask, int W, int P, int key0, int k_end) {
+  uint32_t vis;
+  if (key0 + kAttnTile <= P) {
+    vis = ~0u;
+  } else if (key0 >= P) {
+    const int jb = key0 - P, w = jb >> 5, sh = jb & 31;
+    const uint64_t lo = row_mask[w];
+    const uint64_t hi = w + 1 < W ? row_mask[w + 1] : 0u;
+    vis = static_cast<uint32_t>(((hi << 32) | lo) >> sh);
+  } else {  // the tile straddles P: committed keys, then the first tree bits
+    const int n = P - key0;  // 1 .. 31
+    vis = (row_mask[0] << n) | ((1u << n) - 1u);
+  }
+  const int live = k_end - key0;  // >= 1
+  return live >= kAttnTile ? vis : vis & ((1u << live) - 1u);
+}
 
 // A tile's share of one thread: two 16-byte pieces of keys (key c / 16, dimensions
 // 8 (c % 16) ..) for c = thread, thread + 256, and a pair of keys' 8 dimensions of
@@ -173,25 +193,22 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_partial(AttnArgs a) {
           }
         }
         // scale, mask (committed positions are always visible), online softmax
+        const uint32_t vis = live_row ? tile_visibility(&L.mask[qi * a.W], a.W, a.P, key0, k_end) : 0u;
         float sv[2][4];
         float mx = -INFINITY;
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int pos = key0 + 16 * u + 4 * quarter + r;
-            bool ok = live_row && pos < k_end;
-            if (pos >= a.P) {
-              const int j = pos - a.P;
-              ok = ok && ((L.mask[qi * a.W + min(j >> 5, a.W - 1)] >> (j & 31)) & 1u);
-            }
+            const bool ok = (vis >> (16 * u + 4 * quarter + r)) & 1u;
             sv[u][r] = ok ? st[u][r] * a.scale_log2 : -INFINITY;
             mx = fmaxf(mx, sv[u][r]);
           }
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float mn = fmaxf(m, mx);
-        const float alpha = m == -INFINITY ? 0.f : exp2f(m - mn);
+        // raw 2^x (a probability below 2^-126 flushing to zero does not matter)
+        const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mn);
         // p = hi + lo in bf16; the same two terms feed P.V and the sum
         uint32_t ph[4], pl[4];
         float add = 0.f;
@@ -199,8 +216,8 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_partial(AttnArgs a) {
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int r = 0; r < 4; r += 2) {
-            const float p0 = sv[u][r] == -INFINITY ? 0.f : exp2f(sv[u][r] - mn);
-            const float p1 = sv[u][r + 1] == -INFINITY ? 0.f : exp2f(sv[u][r + 1] - mn);
+            const float p0 = sv[u][r] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sv[u][r] - mn);
+            const float p1 = sv[u][r + 1] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sv[u][r + 1] - mn);
             const uint32_t h = pack_bf16(p0, p1);
             const uint32_t l = pack_bf16(p0 - bf16_lo(h), p1 - bf16_hi(h));
             ph[2 * u + r / 2] = h;
@@ -211,10 +228,14 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_partial(AttnArgs a) {
         m = mn;
         const bf16x8_t pfh = __builtin_bit_cast(bf16x8_t, make_uint4(ph[0], ph[1], ph[2], ph[3]));
         const bf16x8_t pfl = __builtin_bit_cast(bf16x8_t, make_uint4(pl[0], pl[1], pl[2], pl[3]));
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {  // some row's maximum moved
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+        }
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
           const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(&L.vt[buf][16 * dt + col][8 * quarter]);
-          o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfh, o[dt] * alpha, 0, 0, 0);
+          o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfh, o[dt], 0, 0, 0);
           o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl, o[dt], 0, 0, 0);
         }
       }
@@ -225,6 +246,8 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn_partial(AttnArgs a) {
     // the four quarters hold partial sums of the same query
     lsum += __shfl_xor(lsum, 16);
     lsum += __shfl_xor(lsum, 32);
+  }
+  if (live_row) {  // padding rows are never read
     const size_t base = (static_cast<size_t>(g) * a.splits + s) * a.rows_pad + row;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt)
@@ -291,8 +314,11 @@ void attn_plan(int M, int Hq, int Hkv, int P, int T, int* splits, int* tiles_per
   const int tiles = (L + kAttnTile - 1) / kAttnTile;
   // about one workgroup per CU of the 256, at least two tiles each (both in flight at
   // once), so that the partial outputs stay small beside the keys and values read
+#ifndef ATTN_MIN_TILES
+#define ATTN_MIN_TILES 2
+#endif
   int tps = (tiles * Hkv + 255) / 256;
-  if (tps < 2) tps = 2;
+  if (tps < ATTN_MIN_TILES) tps = ATTN_MIN_TILES;
   if (tps > tiles) tps = tiles;
   *tiles_per_split = tps;
   *splits = (tiles + tps - 1) / tps;
