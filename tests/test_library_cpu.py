@@ -182,8 +182,8 @@ def test_tree_plan_shapes():
 
 def test_tree_attention_plan_and_errors_need_no_gpu():
     # Qwen2.5-7B at the last pass of a depth-48 tree: 2336 keys = 73 tiles of 32,
-    # two tiles per range
-    assert ss.subspec_tree_attention_plan(6, 28, 4, 2048, 282) == (37, 2)
+    # three tiles per range
+    assert ss.subspec_tree_attention_plan(6, 28, 4, 2048, 282) == (25, 3)
     for M, Hq, Hkv, P, T in [(6, 28, 4, 0, 0), (1, 1, 1, 0, 0), (6, 40, 8, 30000, 282), (8, 16, 2, 33, 7)]:
         s, t = ss.subspec_tree_attention_plan(M, Hq, Hkv, P, T)
         tiles = -(-(P + T + M) // 32)
