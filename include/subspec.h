@@ -268,6 +268,34 @@ size_t subspec_tree_attention_workspace_bytes(int M, int Hq, int Hkv, int P, int
 int subspec_tree_attention_plan(int M, int Hq, int Hkv, int P, int T, int* splits,
                                 int* tiles_per_split);
 
+/* Cross-layer asynchronous weight prefetch for the verification pass (SubSpec
+ * Sec. 4.3 "Asynchronous Data Transfer", App. E): while the GPU computes with one
+ * offloaded tensor, the next ones are copied from pinned host memory into a fixed
+ * ring of reused device buffers (peak memory does not grow with the model), across
+ * decoder-layer boundaries.
+ *
+ * A prefetcher owns `slots` device buffers of `slot_bytes` each on the device current
+ * at creation, and one copy stream (default priority).  Tickets 0, 1, 2, ... are
+ * handed out in order; ticket t uses slot t % slots.  Per ticket:
+ *   begin    enqueue the host-to-device copy on the copy stream, after the work that
+ *            released the slot's previous ticket (an event on the releasing stream);
+ *   acquire  make `compute` wait for that copy; returns the slot's device pointer,
+ *            valid for work enqueued on `compute` until the ticket is released;
+ *   release  record, on `compute`, that all work using the slot is enqueued.
+ * begin fails with SUBSPEC_EINVAL while the slot's previous ticket is not released
+ * (there is no host-side wait), so a missing release is an error, never a race.
+ * Host sources must be pinned (hipHostMalloc, or torch's pin_memory); the copies are
+ * asynchronous and the host buffer must stay unchanged until the compute stream has
+ * passed the acquire.  Calls on one prefetcher must not overlap in time. */
+typedef struct subspec_prefetch subspec_prefetch;
+int subspec_prefetch_create(size_t slot_bytes, int slots, subspec_prefetch** out);
+int subspec_prefetch_destroy(subspec_prefetch* pf); /* waits for its copies */
+int subspec_prefetch_begin(subspec_prefetch* pf, const void* host_src, size_t bytes,
+                           long long* ticket);
+int subspec_prefetch_acquire(subspec_prefetch* pf, long long ticket, hipStream_t compute,
+                             void** dev_ptr);
+int subspec_prefetch_release(subspec_prefetch* pf, long long ticket, hipStream_t compute);
+
 /* Grow the calling device's workspace to at least `bytes` now (synchronous, may
  * call hipMalloc), so that later calls, e.g. under stream capture, need not. */
 int subspec_reserve(size_t bytes);

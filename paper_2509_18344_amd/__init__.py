@@ -28,6 +28,7 @@ from ._binding import (  # noqa: F401
     subspec_graph_launch,
     subspec_graph_destroy,
     subspec_tree_expand,
+    Prefetcher,
     subspec_tree_attention,
     subspec_tree_attention_plan,
     subspec_tree_attention_workspace_bytes,

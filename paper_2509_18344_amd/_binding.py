@@ -77,6 +77,11 @@ def load_library():
         "subspec_tree_attention": (I, [P, P, P, P, P, P, I, I, I, I, I, I, ctypes.c_float, P, P]),
         "subspec_tree_attention_workspace_bytes": (S, [I, I, I, I, I]),
         "subspec_tree_attention_plan": (I, [I, I, I, I, I, P, P]),
+        "subspec_prefetch_create": (I, [S, I, ctypes.POINTER(ctypes.c_void_p)]),
+        "subspec_prefetch_destroy": (I, [P]),
+        "subspec_prefetch_begin": (I, [P, P, S, ctypes.POINTER(ctypes.c_longlong)]),
+        "subspec_prefetch_acquire": (I, [P, ctypes.c_longlong, P, ctypes.POINTER(ctypes.c_void_p)]),
+        "subspec_prefetch_release": (I, [P, ctypes.c_longlong, P]),
         "subspec_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -230,6 +235,45 @@ def subspec_tree_attention_plan(M, Hq, Hkv, P, T):
     _check("subspec_tree_attention_plan", load_library().subspec_tree_attention_plan(
         M, Hq, Hkv, P, T, ctypes.byref(s), ctypes.byref(t)))
     return s.value, t.value
+
+
+class Prefetcher:
+    """The library's cross-layer weight prefetcher (a ring of `slots` device buffers of
+    `slot_bytes`, one copy stream): begin(host) -> ticket, acquire(ticket, stream) ->
+    device address, release(ticket, stream).  Host sources must be pinned."""
+
+    def __init__(self, slot_bytes: int, slots: int):
+        h = ctypes.c_void_p()
+        _check("subspec_prefetch_create", load_library().subspec_prefetch_create(slot_bytes, slots, ctypes.byref(h)))
+        self._h = h.value
+
+    def begin(self, host, nbytes=None) -> int:
+        if nbytes is None:
+            nbytes = host.numel() * host.element_size()
+        t = ctypes.c_longlong()
+        _check("subspec_prefetch_begin", load_library().subspec_prefetch_begin(self._h, _ptr(host), nbytes,
+                                                                               ctypes.byref(t)))
+        return t.value
+
+    def acquire(self, ticket: int, stream=None) -> int:
+        p = ctypes.c_void_p()
+        _check("subspec_prefetch_acquire", load_library().subspec_prefetch_acquire(self._h, ticket, _stream(stream),
+                                                                                   ctypes.byref(p)))
+        return p.value
+
+    def release(self, ticket: int, stream=None) -> None:
+        _check("subspec_prefetch_release", load_library().subspec_prefetch_release(self._h, ticket, _stream(stream)))
+
+    def close(self) -> None:
+        if self._h:
+            _check("subspec_prefetch_destroy", load_library().subspec_prefetch_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def subspec_tree_plan(R, V, k):

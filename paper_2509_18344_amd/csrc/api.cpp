@@ -727,3 +727,140 @@ int subspec_reserve(size_t bytes) {
 const char* subspec_last_error(void) { return g_last_error.c_str(); }
 
 }  // extern "C"
+
+// --- cross-layer asynchronous weight prefetch (Sec. 4.3, App. E) ---------------------
+
+struct subspec_prefetch {
+  struct Slot {
+    void* dev = nullptr;
+    hipEvent_t copied = nullptr;  // recorded on the copy stream after the copy
+    hipEvent_t freed = nullptr;   // recorded on the releasing stream
+    long long ticket = -1;        // ticket in the slot, -1 if never used
+    bool held = false;            // begun and not yet released
+    bool freed_recorded = false;
+  };
+  int device = 0;
+  size_t slot_bytes = 0;
+  hipStream_t copy = nullptr;
+  std::vector<Slot> slots;
+  long long next = 0;
+};
+
+namespace {
+
+void prefetch_teardown(subspec_prefetch* pf) {
+  if (pf->copy) (void)hipStreamSynchronize(pf->copy);
+  for (auto& s : pf->slots) {
+    if (s.dev) (void)hipFree(s.dev);
+    if (s.copied) (void)hipEventDestroy(s.copied);
+    if (s.freed) (void)hipEventDestroy(s.freed);
+  }
+  if (pf->copy) (void)hipStreamDestroy(pf->copy);
+  delete pf;
+}
+
+// The slot that holds `ticket`, or null (with the error set).
+subspec_prefetch::Slot* prefetch_slot(subspec_prefetch* pf, long long ticket) {
+  if (ticket < 0 || ticket >= pf->next) {
+    fail(SUBSPEC_EINVAL, "prefetch: ticket %lld was not begun", ticket);
+    return nullptr;
+  }
+  auto& s = pf->slots[ticket % static_cast<long long>(pf->slots.size())];
+  if (s.ticket != ticket || !s.held) {
+    fail(SUBSPEC_EINVAL, "prefetch: ticket %lld is released or its slot was reused", ticket);
+    return nullptr;
+  }
+  return &s;
+}
+
+int prefetch_device_check(const subspec_prefetch* pf) {
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != pf->device) return fail(SUBSPEC_EINVAL, "prefetch: created on device %d, called on %d", pf->device, dev);
+  return SUBSPEC_OK;
+}
+
+}  // namespace
+
+int subspec_prefetch_create(size_t slot_bytes, int slots, subspec_prefetch** out) {
+  if (!out) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  *out = nullptr;
+  if (slot_bytes == 0 || slots < 2 || slots > 64)
+    return fail(SUBSPEC_EINVAL, "prefetch: need slot_bytes > 0 and 2 <= slots <= 64");
+  auto* pf = new subspec_prefetch();
+  pf->slot_bytes = slot_bytes;
+  hipError_t e = hipGetDevice(&pf->device);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&pf->copy, hipStreamNonBlocking);
+  pf->slots.resize(slots);
+  for (auto& s : pf->slots) {
+    if (e == hipSuccess) e = hipMalloc(&s.dev, slot_bytes);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&s.copied, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&s.freed, hipEventDisableTiming);
+  }
+  if (e != hipSuccess) {
+    prefetch_teardown(pf);
+    return hip_fail(e, "prefetch_create");
+  }
+  *out = pf;
+  return SUBSPEC_OK;
+}
+
+int subspec_prefetch_destroy(subspec_prefetch* pf) {
+  if (!pf) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  prefetch_teardown(pf);
+  return SUBSPEC_OK;
+}
+
+int subspec_prefetch_begin(subspec_prefetch* pf, const void* host_src, size_t bytes, long long* ticket) {
+  if (!pf || !host_src || !ticket) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (bytes == 0 || bytes > pf->slot_bytes)
+    return fail(SUBSPEC_EINVAL, "prefetch: %zu bytes do not fit a slot of %zu", bytes, pf->slot_bytes);
+  int rc = prefetch_device_check(pf);
+  if (rc) return rc;
+  hipPointerAttribute_t attr{};
+  if (hipPointerGetAttributes(&attr, host_src) != hipSuccess || attr.type != hipMemoryTypeHost) {
+    (void)hipGetLastError();
+    return fail(SUBSPEC_EINVAL, "prefetch: host source must be pinned host memory");
+  }
+  const long long t = pf->next;
+  auto& s = pf->slots[t % static_cast<long long>(pf->slots.size())];
+  if (s.held)
+    return fail(SUBSPEC_EINVAL, "prefetch: slot of ticket %lld still holds ticket %lld (release it first)", t,
+                s.ticket);
+  hipError_t e = hipSuccess;
+  if (s.freed_recorded) e = hipStreamWaitEvent(pf->copy, s.freed, 0);
+  if (e == hipSuccess) e = hipMemcpyAsync(s.dev, host_src, bytes, hipMemcpyHostToDevice, pf->copy);
+  if (e == hipSuccess) e = hipEventRecord(s.copied, pf->copy);
+  if (e != hipSuccess) return hip_fail(e, "prefetch_begin");
+  s.ticket = t;
+  s.held = true;
+  pf->next = t + 1;
+  *ticket = t;
+  return SUBSPEC_OK;
+}
+
+int subspec_prefetch_acquire(subspec_prefetch* pf, long long ticket, hipStream_t compute, void** dev_ptr) {
+  if (!pf || !dev_ptr) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  int rc = prefetch_device_check(pf);
+  if (rc) return rc;
+  auto* s = prefetch_slot(pf, ticket);
+  if (!s) return SUBSPEC_EINVAL;
+  const hipError_t e = hipStreamWaitEvent(compute, s->copied, 0);
+  if (e != hipSuccess) return hip_fail(e, "prefetch_acquire");
+  *dev_ptr = s->dev;
+  return SUBSPEC_OK;
+}
+
+int subspec_prefetch_release(subspec_prefetch* pf, long long ticket, hipStream_t compute) {
+  if (!pf) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  int rc = prefetch_device_check(pf);
+  if (rc) return rc;
+  auto* s = prefetch_slot(pf, ticket);
+  if (!s) return SUBSPEC_EINVAL;
+  const hipError_t e = hipEventRecord(s->freed, compute);
+  if (e != hipSuccess) return hip_fail(e, "prefetch_release");
+  s->held = false;
+  s->freed_recorded = true;
+  return SUBSPEC_OK;
+}

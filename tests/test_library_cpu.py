@@ -211,3 +211,18 @@ def test_tree_attention_plan_and_errors_need_no_gpu():
         call(S=2335)
     with pytest.raises(ss.SubspecError, match="EINVAL"):
         call(scale=float("inf"))
+
+
+def test_prefetch_argument_errors_need_no_gpu():
+    for slot_bytes, slots in [(0, 2), (1024, 1), (1024, 65)]:
+        with pytest.raises(ss.SubspecError, match="EINVAL"):
+            ss.Prefetcher(slot_bytes, slots)
+    lib = ss.load_library()
+    import ctypes
+    t = ctypes.c_longlong()
+    p = ctypes.c_void_p()
+    assert lib.subspec_prefetch_begin(None, None, 16, ctypes.byref(t)) == -1  # SUBSPEC_EINVAL
+    assert lib.subspec_prefetch_acquire(None, 0, None, ctypes.byref(p)) == -1  # SUBSPEC_EINVAL
+    assert lib.subspec_prefetch_release(None, 0, None) == -1  # SUBSPEC_EINVAL
+    assert lib.subspec_prefetch_destroy(None) == -1  # SUBSPEC_EINVAL
+    assert lib.subspec_prefetch_create(16, 2, None) == -1  # SUBSPEC_EINVAL
