@@ -1,6 +1,7 @@
 """Plain fp64 CPU oracle for the low-bit substitute-layer linear (SubSpec, Sec. 4.1)
 and for the draft-tree expansion step with probability sharpening (Sec. 4.2, App. D)
-and the draft model's tree attention over the shared KV cache (Sec. 4.1).
+and the draft model's tree attention over the shared KV cache (Sec. 4.1), and for the
+quantizer with an HQQ-style optimised zero-point (Sec. 4.1, Sec. 5.1).
 
 TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import or call anything in this package.
@@ -33,4 +34,7 @@ from .tree_attn import (  # noqa: F401
     append_kv,
     tree_attention,
     weighted_abs_v,
+)
+from .hqq import (  # noqa: F401
+    quantize_hqq,
 )
