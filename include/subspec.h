@@ -112,6 +112,20 @@ int subspec_quantize(const float* w, int bits, int group, int N, int K,
                      uint8_t* codes, uint16_t* scales, uint16_t* zeros,
                      hipStream_t stream);
 
+/* Same contract and outputs as subspec_quantize, with the zero of every group
+ * optimised as in HQQ, the data-free quantizer SubSpec uses for its substitutes
+ * (Sec. 4.1; 4-bit, groups of 64, Sec. 5.1).  The paper gives no algorithm; this
+ * follows the cited half-quadratic quantization work: the scale stays the min/max
+ * scale; from the min/max zero, rounds of (quantize with z; e = sign(x) max(|x| -
+ * |x|^(p-1)/beta, 0) for x = w - s (q - z); z = mean(q - (w - e) / s)) with p = 0.7,
+ * beta = 10 growing by 1.01 per round, at most 20 rounds, keep the zero with the
+ * smallest sum |w - s (q - z)| and stop at the first round that does not improve it.
+ * The best zero (fp16) replaces the min/max zero only if it is still better in fp16,
+ * so no group's error grows.  float64 throughout, sums in index order. */
+int subspec_quantize_hqq(const float* w, int bits, int group, int N, int K,
+                         uint8_t* codes, uint16_t* scales, uint16_t* zeros,
+                         hipStream_t stream);
+
 /* Pack one-byte codes (device uint8 [N][K], each < 2^bits) into the tile layout
  * above (device, subspec_qpack_bytes() bytes, written).  Codes with bits above
  * `bits` set are masked off. */

@@ -22,6 +22,7 @@ from ._binding import (  # noqa: F401
     subspec_qpack_bytes,
     subspec_qpack_host,
     subspec_quantize,
+    subspec_quantize_hqq,
     subspec_reserve,
     subspec_stack_forward,
     subspec_stack_capture,

@@ -60,6 +60,7 @@ def load_library():
         "subspec_qpack_bytes": (S, [I, I, I]),
         "subspec_quantize": (I, [P, I, I, I, I, P, P, P, P]),
         "subspec_qpack": (I, [P, I, I, I, P, P]),
+        "subspec_quantize_hqq": (I, [P, I, I, I, I, P, P, P, P]),
         "subspec_qpack_host": (I, [P, I, I, I, P]),
         "subspec_qlinear": (I, [P, P, P, P, I, I, I, I, I, P, P]),
         "subspec_qlinear_path": (I, [P, P, P, P, I, I, I, I, I, P, I, P]),
@@ -130,6 +131,11 @@ def subspec_qpack_bytes(bits: int, N: int, K: int) -> int:
 
 def subspec_quantize(w, bits, group, N, K, codes, scales, zeros, stream=None) -> int:
     return _check("subspec_quantize", load_library().subspec_quantize(
+        _ptr(w), bits, group, N, K, _ptr(codes), _ptr(scales), _ptr(zeros), _stream(stream)))
+
+
+def subspec_quantize_hqq(w, bits, group, N, K, codes, scales, zeros, stream=None) -> int:
+    return _check("subspec_quantize_hqq", load_library().subspec_quantize_hqq(
         _ptr(w), bits, group, N, K, _ptr(codes), _ptr(scales), _ptr(zeros), _stream(stream)))
 
 

@@ -17,6 +17,7 @@
 #include "kernels.h"
 #include "kernels_tree.h"
 #include "kernels_attn.h"
+#include "kernels_hqq.h"
 
 namespace {
 
@@ -450,6 +451,19 @@ int subspec_quantize(const float* w, int bits, int group, int N, int K, uint8_t*
     return fail(SUBSPEC_EINVAL, "device pointers must be 16-byte aligned");
   hipError_t e = subspec::launch_quantize(w, bits, group, N, K, codes, scales, zeros, stream);
   if (e != hipSuccess) return hip_fail(e, "quantize launch");
+  return SUBSPEC_OK;
+}
+
+int subspec_quantize_hqq(const float* w, int bits, int group, int N, int K, uint8_t* codes,
+                         uint16_t* scales, uint16_t* zeros, hipStream_t stream) {
+  int rc = check_bits_group(bits, group);
+  if (rc) return rc;
+  if (N <= 0 || K <= 0 || K % group) return fail(SUBSPEC_EINVAL, "N=%d K=%d group=%d: bad shape", N, K, group);
+  if (!w || !codes || !scales || !zeros) return fail(SUBSPEC_EINVAL, "null pointer argument");
+  if (!aligned16(w) || !aligned16(codes) || !aligned16(scales) || !aligned16(zeros))
+    return fail(SUBSPEC_EINVAL, "device pointers must be 16-byte aligned");
+  hipError_t e = subspec::launch_quantize_hqq(w, bits, group, N, K, codes, scales, zeros, stream);
+  if (e != hipSuccess) return hip_fail(e, "quantize_hqq launch");
   return SUBSPEC_OK;
 }
 

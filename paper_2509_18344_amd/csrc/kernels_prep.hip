@@ -1,7 +1,9 @@
-// Weight preparation kernels: min/max quantizer, packer into the tile layout and
-// the materialising dequantizer (include/subspec.h documents each operation).
+// Weight preparation kernels: min/max quantizer, the quantizer with an HQQ-style
+// optimised zero-point, packer into the tile layout and the materialising
+// dequantizer (include/subspec.h documents each operation).
 #include "device_common.h"
 #include "kernels.h"
+#include "kernels_hqq.h"
 
 namespace subspec {
 
@@ -87,6 +89,113 @@ __global__ __launch_bounds__(256) void k_quantize(const float* __restrict__ w, i
     sc[static_cast<long long>(g) * N + n] = s16;
     zr[static_cast<long long>(g) * N + n] = z16;
   }
+}
+
+// HQQ-style zero-point (SubSpec Sec. 4.1 and 5.1 quantize the substitutes with HQQ;
+// the rounds follow the cited half-quadratic quantization work).  The scale is the
+// min/max scale; starting from the min/max zero, each round quantizes with the
+// current zero, shrinks the residual x = w - s (q - z) with the generalised soft
+// threshold sign(x) max(|x| - |x|^(p-1) / beta, 0) and refits the zero as the mean of
+// q - (w - e) / s; the group's sum of |w - s (q - z)| decides: the best zero is kept
+// and a round without improvement ends the search; beta grows by kappa per round.
+// The best zero, rounded to fp16, replaces the min/max zero only if it is still
+// better in fp16.  Everything in float64 with sums in index order, one thread per
+// (column n, group g), so that the rounding decisions are reproducible.
+constexpr double kHqqP = 0.7;
+constexpr double kHqqBeta = 10.0;
+constexpr double kHqqKappa = 1.01;
+constexpr int kHqqIters = 20;
+
+// The group's weights sit in LDS, transposed (element i of thread t at [i][t]), so
+// the rounds index them without spilling registers and without bank conflicts.
+template <int GROUP>
+__global__ __launch_bounds__(kWave) void k_quantize_hqq(const float* __restrict__ w, int bits, int N, int K,
+                                                       uint8_t* __restrict__ codes, uint16_t* __restrict__ sc,
+                                                       uint16_t* __restrict__ zr) {
+  __shared__ float wl[GROUP][kWave];
+  const int t = threadIdx.x;
+  const int gpr = K / GROUP;
+  const long long gid = static_cast<long long>(blockIdx.x) * kWave + t;  // g * N + n
+  if (gid >= static_cast<long long>(N) * gpr) return;  // no barrier follows
+  const long long n = gid % N;
+  const int g = static_cast<int>(gid / N);
+  const float* src = w + n * K + static_cast<long long>(g) * GROUP;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int i = 0; i < GROUP; i += 4) {
+    const float4 q4 = *reinterpret_cast<const float4*>(src + i);
+    wl[i][t] = q4.x;
+    wl[i + 1][t] = q4.y;
+    wl[i + 2][t] = q4.z;
+    wl[i + 3][t] = q4.w;
+    mn = fminf(fminf(mn, q4.x), fminf(fminf(q4.y, q4.z), q4.w));
+    mx = fmaxf(fmaxf(mx, q4.x), fmaxf(fmaxf(q4.y, q4.z), q4.w));
+  }
+  const double wmin = mn, wmax = mx;
+  const double qmax = static_cast<double>((1 << bits) - 1);
+  uint16_t s16 = f64_to_f16_bits((wmax - wmin) / qmax);
+  double s = f16_bits_to_f64(s16);
+  const bool degenerate = (wmax == wmin) || (s == 0.0);
+  uint16_t z16;
+  if (degenerate) {
+    s16 = 0x3C00u;
+    s = 1.0;
+    z16 = f64_to_f16_bits(-wmin);
+  } else {
+    z16 = f64_to_f16_bits(-wmin / s);
+  }
+  auto code = [&](double x, double z) __attribute__((always_inline)) {
+    const double c = __builtin_rint(x / s + z);
+    return c < 0.0 ? 0.0 : (c > qmax ? qmax : c);
+  };
+  auto l1 = [&](double z) __attribute__((always_inline)) {
+    double tot = 0.0;
+    for (int i = 0; i < GROUP; ++i) {
+      const double x = wl[i][t];
+      tot += fabs(x - (code(x, z) - z) * s);
+    }
+    return tot;
+  };
+  if (!degenerate) {
+    const double z0 = f16_bits_to_f64(z16);
+    const double e0 = l1(z0);
+    double z = z0, best_z = z0, best = e0, beta = kHqqBeta;
+    for (int it = 0; it < kHqqIters; ++it) {
+      double acc = 0.0;
+      for (int i = 0; i < GROUP; ++i) {
+        const double x = wl[i][t];
+        const double q = code(x, z);
+        const double r = x - (q - z) * s;
+        const double a = fabs(r);
+        const double e = r == 0.0 ? 0.0 : copysign(fmax(a - pow(a, kHqqP - 1.0) / beta, 0.0), r);
+        acc += q - (x - e) / s;
+      }
+      const double z_new = acc / GROUP;
+      const double err = l1(z_new);
+      if (!(err < best)) break;
+      best = err;
+      best_z = z_new;
+      z = z_new;
+      beta = beta * kHqqKappa;
+    }
+    const uint16_t zb = f64_to_f16_bits(best_z);
+    if (l1(f16_bits_to_f64(zb)) < e0) z16 = zb;
+  }
+  const double zf = f16_bits_to_f64(z16);
+  uint8_t* dst = codes + n * K + static_cast<long long>(g) * GROUP;
+  for (int i = 0; i < GROUP; i += 16) {
+    uint32_t word[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t b = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        b |= (degenerate ? 0u : static_cast<uint32_t>(code(wl[i + 4 * j + k][t], zf))) << (8 * k);
+      word[j] = b;
+    }
+    *reinterpret_cast<uint4*>(dst + i) = make_uint4(word[0], word[1], word[2], word[3]);
+  }
+  sc[static_cast<long long>(g) * N + n] = s16;
+  zr[static_cast<long long>(g) * N + n] = z16;
 }
 
 // Packed words of one slice from its 32 codes c[e + 8*j] (k order of the slice).
@@ -192,6 +301,17 @@ hipError_t launch_quantize(const float* w, int bits, int group, int N, int K, ui
   else
     hipLaunchKernelGGL(k_quantize<128>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, w,
                        bits, N, K, codes, sc, zr);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_hqq(const float* w, int bits, int group, int N, int K, uint8_t* codes,
+                               uint16_t* sc, uint16_t* zr, hipStream_t st) {
+  const long long groups = static_cast<long long>(N) * (K / group);
+  const dim3 grid(static_cast<unsigned>((groups + kWave - 1) / kWave)), block(kWave);
+  if (group == 64)
+    hipLaunchKernelGGL(k_quantize_hqq<64>, grid, block, 0, st, w, bits, N, K, codes, sc, zr);
+  else
+    hipLaunchKernelGGL(k_quantize_hqq<128>, grid, block, 0, st, w, bits, N, K, codes, sc, zr);
   return hipGetLastError();
 }
 

@@ -226,3 +226,14 @@ def test_prefetch_argument_errors_need_no_gpu():
     assert lib.subspec_prefetch_release(None, 0, None) == -1  # SUBSPEC_EINVAL
     assert lib.subspec_prefetch_destroy(None) == -1  # SUBSPEC_EINVAL
     assert lib.subspec_prefetch_create(16, 2, None) == -1  # SUBSPEC_EINVAL
+
+
+def test_quantize_hqq_argument_errors_need_no_gpu():
+    with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
+        ss.subspec_quantize_hqq(16, 5, 64, 16, 128, 16, 16, 16, stream=0)
+    with pytest.raises(ss.SubspecError, match="EINVAL"):
+        ss.subspec_quantize_hqq(16, 4, 64, 16, 100, 16, 16, 16, stream=0)
+    with pytest.raises(ss.SubspecError, match="EINVAL"):
+        ss.subspec_quantize_hqq(None, 4, 64, 16, 128, 16, 16, 16, stream=0)
+    with pytest.raises(ss.SubspecError, match="EINVAL"):
+        ss.subspec_quantize_hqq(16, 4, 64, 16, 128, 24, 16, 16, stream=0)
