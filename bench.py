@@ -32,7 +32,9 @@ tokens: the last pass of a depth-48 tree).  Their traffic files are
 profiles/traffic_tree.json and profiles/traffic_attn.json.  ``--workload prefetch``
 times the target's verification pass over offloaded Qwen2.5-7B layers (bf16
 weights in pinned host memory, 289 tree tokens) with the cross-layer prefetcher,
-against copies alone, GEMMs alone and copy-then-compute.
+against copies alone, GEMMs alone and copy-then-compute.  ``--workload hqq`` times the
+quantizer with an HQQ-style optimised zero-point on one Qwen2.5-7B layer (4-bit,
+groups of 64), beside the min/max quantizer.
 """
 from __future__ import annotations
 
@@ -78,7 +80,7 @@ def parse():
                          "or tree_expand (the draft-tree expansion step; --ms gives its rows) "
                          "or tree_attn (one layer's tree attention over the shared KV cache) "
                          "or prefetch (verification pass over offloaded layers with cross-layer "
-                         "weight prefetch)")
+                         "weight prefetch) or hqq (HQQ-style quantization of one Qwen2.5-7B layer)")
     ap.add_argument("--ms", default=None, help="comma-separated M values (default: the workload's)")
     ap.add_argument("--rotate-gb", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -497,6 +499,9 @@ def main():
     if args.workload == "prefetch":
         run_prefetch(args, torch, ss)
         return
+    if args.workload == "hqq":
+        run_hqq(args, torch, ss)
+        return
     wl = WORKLOADS[args.workload]
     ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else wl.ms
     stream = torch.cuda.Stream()
@@ -914,6 +919,77 @@ def run_prefetch(args, torch, ss):
         "copy_only_GBs": round(copy_gbs, 2),
         "gemm_hidden_frac": round((t_serial - t_slots[PF_SLOTS]) / t_gemm, 3) if t_gemm > 0 else None,
     }
+    line = json.dumps(out)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(line + "\n")
+    print(line, flush=True)
+
+
+
+def hqq_cpu_baseline(min_seconds=10.0):
+    """The fp64 oracle's HQQ quantizer on 1024 x 3584 weights, repeated for min_seconds."""
+    import oracle
+    from paper_2509_18344_amd import synth
+    w = synth.weights_np(1024, 3584, 51)
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.quantize_hqq(w, 4, 64)
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    n = steps * w.size
+    return {"value": round(n / dt / 1e6, 3), "unit": "M weights/s", "cores": 1, "kind": "oracle",
+            "seconds": round(dt, 3),
+            "sample": f"{steps} x 1024 x 3584 fp32 weights, 4-bit g64 (NumPy fp64, one thread)"}
+
+
+def run_hqq(args, torch, ss):
+    """One step = quantizing the 7 projections of one Qwen2.5-7B layer (233 M fp32
+    weights, on the device) to 4 bits, groups of 64, with the optimised zero."""
+    from paper_2509_18344_amd import synth
+    bits, group = 4, 64
+    ws, outs = [], []
+    for i, (_, n, k) in enumerate(PF_PROJS):
+        w = synth.weights_torch(n, k, 61, i)
+        ws.append(w)
+        outs.append((torch.empty((n, k), dtype=torch.uint8, device="cuda"),
+                     torch.empty((k // group, n), dtype=torch.float16, device="cuda"),
+                     torch.empty((k // group, n), dtype=torch.float16, device="cuda")))
+    stream = torch.cuda.Stream()
+    n_weights = sum(n * k for _, n, k in PF_PROJS)
+
+    def step_with(fn):
+        def step(_s):
+            for (name, n, k), w, (c, sc, zr) in zip(PF_PROJS, ws, outs):
+                fn(w, bits, group, n, k, c, sc, zr, stream)
+        return step
+
+    with torch.cuda.stream(stream):
+        total_ms = timed(torch, stream, step_with(ss.subspec_quantize_hqq), args.warmup, args.steps)
+        mm_ms = timed(torch, stream, step_with(ss.subspec_quantize), 1, max(3, args.steps))
+    ms = total_ms / args.steps
+    mm = mm_ms / max(3, args.steps)
+    nbytes = n_weights * (4 + 1) + 2 * 2 * n_weights // group  # fp32 in, codes, fp16 scale and zero out
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    out = {
+        "metric": "weights quantized per second with the HQQ-style optimised zero-point (one Qwen2.5-7B layer, "
+                  "4-bit, groups of 64)",
+        "value": round(n_weights / (ms * 1e-3) / 1e9, 3), "unit": "G weights/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic: N(0,0.02) fp32 weights generated on the device, seeded",
+        "config": {"workload": "HQQ-style quantization of the 7 projections of one Qwen2.5-7B layer, 4-bit g64",
+                   "weights": n_weights, "minmax_ms_per_step": round(mm, 3), "timing": "eager launches"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "k_quantize_hqq<64> (7 launches per step)", "alg_bytes_per_step": nbytes,
+                     "note": "float64 arithmetic (a power per weight and round) bounds it, not HBM"},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = hqq_cpu_baseline()
     line = json.dumps(out)
     if args.json_out:
         with open(args.json_out, "w") as f:
