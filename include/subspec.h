@@ -45,6 +45,15 @@
  *    contiguous run, and every pair unpacks with a shift and one and-or into two
  *    16-bit fields.
  *  - Scales and zeros are fp16 arrays [K/group][N], row-major (s[g][n] at g*N + n).
+ *
+ * Around the substitute linear the library also provides, each declared below with
+ * its own contract: the draft-tree expansion with probability sharpening
+ * (subspec_tree_*, Sec. 4.2 and App. D), the draft's tree attention over the key/value
+ * cache it shares with the target (subspec_tree_attention*, Sec. 4.1), the
+ * verification pass's cross-layer asynchronous weight prefetch (subspec_prefetch_*,
+ * Sec. 4.3 and App. E) and the quantizer with an HQQ-style optimised zero-point
+ * (subspec_quantize_hqq, Sec. 4.1 and 5.1).  The shape limits listed above are the
+ * substitute linear's; the other calls state theirs.
  */
 #ifndef SUBSPEC_H_
 #define SUBSPEC_H_
