@@ -197,11 +197,13 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   };
   int resident = resident_of(c);
   // Two tiles per wavefront halve the workgroups, and each A fragment read from LDS
-  // feeds two MFMAs.  From two row tiles on, that LDS traffic is what bounds a
-  // workgroup, so two tiles win whenever they still leave every CU a column group and
-  // two wavefronts per SIMD (measured on the 7B gate|up at M = 32 and 64; at eight row
-  // tiles the two-tile variant fits one wavefront per SIMD and loses).  With one row
-  // tile they only pay when the one-tile launch would need a second residency round.
+  // feeds two MFMAs.  At two row tiles that LDS traffic is what bounds a workgroup, so
+  // two tiles win whenever they still leave every CU a column group and two
+  // wavefronts per SIMD (measured on the 7B gate|up at M = 32).  At four row tiles the
+  // one-tile kernel reads its A fragments a step ahead and is faster (7B gate|up at
+  // M = 64: 36.7 against 38.4 us); at eight row tiles the two-tile variant fits one
+  // wavefront per SIMD and loses.  Otherwise two tiles only pay when the one-tile
+  // launch would need a second residency round.
   if (c.path == 2 && !tu.mfma_nt) {
     subspec::KernelChoice c2 = c;
     c2.nt = 2;
@@ -209,7 +211,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
       const int r2 = resident_of(c2);
       const long long rounds1 = (groups_of(c) + resident - 1) / resident;
       const long long rounds2 = (groups_of(c2) + r2 - 1) / r2;
-      const bool lds_bound = c.rows >= 32 && groups_of(c2) >= device_cus() && r2 >= 2 * device_cus();
+      const bool lds_bound = c.rows == 32 && groups_of(c2) >= device_cus() && r2 >= 2 * device_cus();
       if (lds_bound || (groups_of(c) > resident && rounds2 < rounds1)) {
         c = c2;
         resident = r2;

@@ -288,6 +288,11 @@ struct MfmaBody {
   static constexpr int GPC = CH * GPB;        // groups per chunk
   static constexpr int PIECES = ROWS * CH * 16;
   static constexpr int PPT = PIECES / THREADS;  // pieces per thread per chunk
+  // A-fragment prefetch (see compute) for two or four row tiles with one tile per
+  // wavefront: measured -1.7 us on the 7B gate|up at M = 64 and -1 us on down at
+  // M = 32.  The two-tile and eight-row-tile variants would need more than 256 VGPRs
+  // with it (one wavefront per SIMD), and the one-row-tile one gains nothing.
+  static constexpr bool kPrefetchA = (MT == 2 || MT == 4) && NT == 1;
   static_assert(PIECES % THREADS == 0, "a chunk is a whole number of pieces per thread");
   using Lds = MfmaLds<ROWS, CH, GPC>;
   struct W {
@@ -403,13 +408,32 @@ struct MfmaBody {
           // (gate|up M = 32), so that variant keeps the normal priority.
           constexpr bool kRaisePrio = !(MT == 2 && NT == 2);
           if constexpr (kRaisePrio) __builtin_amdgcn_s_setprio(1);
+          // With kPrefetchA the A fragments of the next 32-k step are read before the
+          // MFMAs of the current one, and scheduling fences keep the compiler from
+          // sinking those reads back next to their first use, so the LDS latency runs
+          // under four or eight MFMAs instead of stalling the wavefront.
+          bf16x8_t Acur[MT];
+          if constexpr (kPrefetchA) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              Acur[mt] = __builtin_bit_cast(bf16x8_t, L.x[buf][slot(16 * mt + col, b, 4 * (gi * SPG) + quarter)]);
+          }
 #pragma unroll
           for (int js = 0; js < SPG; ++js) {
             const int j = gi * SPG + js;
+            bf16x8_t Anext[MT];
+            if constexpr (kPrefetchA) {
+              if (js + 1 < SPG) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                  Anext[mt] = __builtin_bit_cast(bf16x8_t, L.x[buf][slot(16 * mt + col, b, 4 * (j + 1) + quarter)]);
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
             static_for<MT>([&](auto mtc) __attribute__((always_inline)) {
               constexpr int mt = decltype(mtc)::value;
-              const bf16x8_t A = __builtin_bit_cast(
-                  bf16x8_t, L.x[buf][slot(16 * mt + col, b, 4 * j + quarter)]);
+              const bf16x8_t A = kPrefetchA ? Acur[mt]
+                                            : __builtin_bit_cast(bf16x8_t, L.x[buf][slot(16 * mt + col, b, 4 * j + quarter)]);
 #pragma unroll
               for (int t = 0; t < NT; ++t) {
                 const uint4 bw = make_uint4(pr[t][4 * j], pr[t][4 * j + 1], pr[t][4 * j + 2],
@@ -424,6 +448,13 @@ struct MfmaBody {
                                                                   0, 0, 0);
               }
             });
+            if constexpr (kPrefetchA) {
+              __builtin_amdgcn_sched_barrier(0);
+              if (js + 1 < SPG) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) Acur[mt] = Anext[mt];
+              }
+            }
           }
           if constexpr (kRaisePrio) __builtin_amdgcn_s_setprio(0);
           float sv[NT];
