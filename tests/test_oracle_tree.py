@@ -110,3 +110,50 @@ def test_invariants():
     mask[pi, tok] = False
     assert s[mask].max() <= sc[-1]
     assert oracle.kth_gap(bits, parent, 0.2, k) >= 0
+
+
+def _brute_gap(bits, parent, T, k):
+    # pure-Python scores and a plain sort, independent of numpy's sorting
+    vals = oracle.bf16_bits_to_f64(bits)
+    R, V = vals.shape
+    scores = []
+    for i in range(R):
+        z = [float(vals[i, v]) / T for v in range(V)]
+        m = max(z)
+        lse = m + math.log(sum(math.exp(t - m) for t in z))
+        scores += [float(parent[i]) + t - lse for t in z]
+    scores.sort(reverse=True)
+    return scores[k - 1] - scores[k] if len(scores) > k else math.inf
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_kth_gap_brute_force_tiny(seed):
+    rng = np.random.default_rng(400 + seed)
+    R, V = int(rng.integers(1, 4)), int(rng.integers(2, 7))
+    k = int(rng.integers(1, R * V))
+    bits = _bf16(rng.normal(0, 2, (R, V)))
+    parent = rng.normal(-1, 1, R)
+    T = [0.2, 1.0, 0.5][seed % 3]
+    got = oracle.kth_gap(bits, parent, T, k)
+    want = _brute_gap(bits, parent, T, k)
+    assert got > 0 and math.isclose(got, want, rel_tol=1e-9, abs_tol=1e-12)
+
+
+def test_kth_gap_tie_and_full_selection():
+    # two equal rows under equal parents: every candidate appears twice, so the
+    # gap after an odd k is an exact tie (0) and after an even k it is positive
+    rng = np.random.default_rng(9)
+    row = rng.normal(0, 2, 6)
+    bits = _bf16(np.stack([row, row]))
+    parent = np.array([-0.5, -0.5])
+    assert oracle.kth_gap(bits, parent, 0.2, 1) == 0.0
+    assert oracle.kth_gap(bits, parent, 0.2, 3) == 0.0
+    g2 = oracle.kth_gap(bits, parent, 0.2, 2)
+    assert g2 > 0 and math.isclose(g2, _brute_gap(bits, parent, 0.2, 2), rel_tol=1e-9)
+    # uniform logits: all scores of a row tie; the gap between rows is the parent gap
+    ub = _bf16(np.full((2, 5), 0.75))
+    assert oracle.kth_gap(ub, np.array([-1.0, -3.0]), 0.2, 2) == 0.0
+    assert math.isclose(oracle.kth_gap(ub, np.array([-1.0, -3.0]), 0.2, 5), 2.0, abs_tol=1e-13)
+    # k = R * V: nothing is left out of the selection
+    assert oracle.kth_gap(bits, parent, 0.2, 12) == math.inf
+    assert oracle.kth_gap(ub, np.array([-1.0, -3.0]), 0.2, 10) == math.inf

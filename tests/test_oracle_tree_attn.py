@@ -155,3 +155,84 @@ def test_brute_force_tiny(seed):
             want = [sum(w[j] * vals[j][d] for j in range(len(w))) / tot for d in range(D)]
             assert np.allclose(out[i, h], want, atol=1e-12), (seed, i, h)
     assert list(visible_positions(mask, 0, P, T, M))[:P] == list(range(P))
+
+
+@pytest.mark.parametrize("M,Hq,Hkv,D,P,T,k,qs", [(6, 28, 4, 16, 40, 12, 6, 1.0), (3, 6, 3, 16, 33, 7, 4, 2.0)])
+def test_weighted_abs_v_matches_library_sdpa_on_abs_values(M, Hq, Hkv, D, P, T, k, qs):
+    # sum_j p_j |v_j| is attention with the values replaced by their magnitudes:
+    # the library routine on |V| must give the same numbers (pins the weights p_j,
+    # the gather of visible keys and the head grouping of weighted_abs_v).
+    x, mask = _case(M, Hq, Hkv, D, P, T, k, 11 + P + T, q_scale=qs)
+    scale = 1.0 / math.sqrt(D)
+    wabs = oracle.weighted_abs_v(x["q"], x["k_cache"], x["v_cache"], P, T, x["k_new"], x["v_new"], mask, scale)
+    _, kc, vc = tree_attention(x["q"], x["k_cache"], x["v_cache"], P, T, x["k_new"], x["v_new"], mask, scale)
+    L = P + T + M
+    q = torch.from_numpy(oracle.bf16_bits_to_f64(x["q"])).permute(1, 0, 2)[None]
+    K = torch.from_numpy(oracle.bf16_bits_to_f64(kc[:, :L])).repeat_interleave(Hq // Hkv, 0)[None]
+    V = torch.from_numpy(np.abs(oracle.bf16_bits_to_f64(vc[:, :L]))).repeat_interleave(Hq // Hkv, 0)[None]
+    allow = np.zeros((M, L), dtype=bool)
+    allow[:, :P] = True
+    for i in range(M):
+        for j in range(T + M):
+            allow[i, P + j] = (int(mask[i, j >> 5]) >> (j & 31)) & 1 == 1
+    ref = torch.nn.functional.scaled_dot_product_attention(q, K, V, attn_mask=torch.from_numpy(allow),
+                                                           scale=scale)
+    assert np.allclose(wabs, ref[0].permute(1, 0, 2).numpy(), atol=1e-12, rtol=0)
+
+
+def test_weighted_abs_v_bounds_and_sign_cases():
+    M, Hq, Hkv, D, P, T, k = 4, 6, 2, 8, 17, 9, 4
+    x, mask = _case(M, Hq, Hkv, D, P, T, k, 23)
+    scale = 1.0 / math.sqrt(D)
+    args = (x["q"], x["k_cache"], x["v_cache"], P, T, x["k_new"], x["v_new"], mask, scale)
+    out, _, _ = tree_attention(*args)
+    wabs = oracle.weighted_abs_v(*args)
+    # triangle inequality: |sum p v| <= sum p |v|, with p_j >= 0 summing to one
+    assert (np.abs(out) <= wabs + 1e-15).all()
+    assert (wabs >= 0).all()
+    # values of one sign: the bound is attained (|v| = v or -v everywhere)
+    vc_pos = x["v_cache"] & np.uint16(0x7FFF)  # clear the bf16 sign bits
+    vn_pos = x["v_new"] & np.uint16(0x7FFF)
+    args_pos = (x["q"], x["k_cache"], vc_pos, P, T, x["k_new"], vn_pos, mask, scale)
+    out_pos, _, _ = tree_attention(*args_pos)
+    assert np.allclose(oracle.weighted_abs_v(*args_pos), out_pos, atol=1e-14, rtol=0)
+    neg = lambda b: b ^ np.uint16(0x8000)
+    args_neg = (x["q"], x["k_cache"], neg(vc_pos), P, T, x["k_new"], neg(vn_pos), mask, scale)
+    out_neg, _, _ = tree_attention(*args_neg)
+    assert np.allclose(oracle.weighted_abs_v(*args_neg), -out_neg, atol=1e-14, rtol=0)
+    # constant values c: the weighted magnitude is |c| whatever the weights
+    c = oracle.bf16_round_bits(np.full(x["v_cache"].shape, -0.375, np.float32))
+    cn = oracle.bf16_round_bits(np.full(x["v_new"].shape, -0.375, np.float32))
+    wc = oracle.weighted_abs_v(x["q"], x["k_cache"], c, P, T, x["k_new"], cn, mask, scale)
+    assert np.allclose(wc, 0.375, atol=1e-15, rtol=0)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_weighted_abs_v_brute_force_tiny(seed):
+    rng = np.random.default_rng(300 + seed)
+    M, Hkv, G, D = int(rng.integers(1, 4)), int(rng.integers(1, 3)), int(rng.integers(1, 3)), 4
+    P, T = int(rng.integers(0, 4)), int(rng.integers(0, 5))
+    Hq = Hkv * G
+    x = synth.tree_attn_inputs(M, Hq, Hkv, D, P + T + M, seed + 70)
+    mask = rng.integers(0, 2 ** 31, (M, 1)).astype(np.uint32)
+    for i in range(M):
+        mask[i, 0] |= np.uint32(1 << (T + i))
+    scale = 0.9
+    wabs = oracle.weighted_abs_v(x["q"], x["k_cache"], x["v_cache"], P, T, x["k_new"], x["v_new"], mask, scale)
+    f = oracle.bf16_bits_to_f64
+    for i in range(M):
+        for h in range(Hq):
+            g = h // G
+            keys, vals = [], []
+            for t in range(P + T + M):
+                if t >= P and not (int(mask[i, 0]) >> (t - P)) & 1:
+                    continue
+                src_k = f(x["k_new"][t - P - T, g]) if t >= P + T else f(x["k_cache"][g, t])
+                src_v = f(x["v_new"][t - P - T, g]) if t >= P + T else f(x["v_cache"][g, t])
+                keys.append(sum(float(a) * float(b) for a, b in zip(f(x["q"][i, h]), src_k)) * scale)
+                vals.append([abs(float(v)) for v in src_v])
+            mx = max(keys)
+            w = [math.exp(s - mx) for s in keys]
+            tot = sum(w)
+            want = [sum(w[j] * vals[j][d] for j in range(len(w))) / tot for d in range(D)]
+            assert np.allclose(wabs[i, h], want, atol=1e-12), (seed, i, h)
