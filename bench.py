@@ -58,8 +58,9 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 # and which kernel names belong to it.
 FAMILIES = {
     "qlinear": {"json": os.path.join(ROOT, "profiles", "traffic.json"),
-                "sources": ("kernels_qlinear.hip", "device_common.h", "kernels.h"),
-                "kernels": ("k_qgemv", "k_qgemm_mfma")},
+                "sources": ("kernels_qlinear.hip", "kernels_qmma.hip", "qmma_kernel.h", "qlinear_device.h",
+                            "device_common.h", "kernels.h"),
+                "kernels": ("k_qgemv", "k_qgemm_mfma", "k_qmma")},
     "tree": {"json": os.path.join(ROOT, "profiles", "traffic_tree.json"),
              "sources": ("kernels_tree.hip", "kernels_tree.h", "device_common.h", "kernels.h"),
              "kernels": ("k_tree_expand",)},
@@ -119,10 +120,14 @@ def dispatch_key(family: str, targs, grid_items: int, wg_items: int) -> str:
 def plan_key(plan, bits, group) -> str:
     wg = plan["waves"] * 64
     if plan["path"] == 1:
-        family, rows = "k_qgemv", plan["rows"]
+        family = "k_qgemv"
+        targs = (bits, group, plan["rows"], plan["tiles_per_wave"], plan["chunk_blocks"], plan["waves"])
+    elif plan["mfma_rows"] == 32:
+        family = "k_qmma"
+        targs = (bits, group, plan["rows"] // 32, plan["tiles_per_wave"] // 2, plan["ring_chunks"])
     else:
-        family, rows = "k_qgemm_mfma", plan["rows"] // 16
-    targs = (bits, group, rows, plan["tiles_per_wave"], plan["chunk_blocks"], plan["waves"])
+        family = "k_qgemm_mfma"
+        targs = (bits, group, plan["rows"] // 16, plan["tiles_per_wave"], plan["chunk_blocks"], plan["waves"])
     return dispatch_key(family, targs, plan["grid"] * wg, wg)
 
 
@@ -207,7 +212,7 @@ def summarize_trace(d):
                     continue
                 targs = [int(a) for a in m.group(2)[1:-1].split(",")] if m.group(2) else []
                 name = m.group(1)
-                if name in ("k_qgemv", "k_qgemm_mfma"):
+                if name in ("k_qgemv", "k_qgemm_mfma", "k_qmma"):
                     key = dispatch_key(name, targs, int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
                 else:
                     key = f"{m.group(0)} grid={r['Grid_Size_X']} wg={r['Workgroup_Size_X']}"

@@ -82,16 +82,27 @@ enum subspec_path {
   SUBSPEC_PATH_GEMV = 1, /* VALU dot products; the four 16-lane quarters of a
                             wavefront split K and are summed with lane shuffles,
                             per-group sums of x reduced with DPP; M <= 8          */
-  SUBSPEC_PATH_MFMA = 2  /* bf16 matrix cores on unpacked code tiles; any M        */
+  SUBSPEC_PATH_MFMA = 2, /* bf16 matrix cores on unpacked code tiles; any M; the
+                            plan picks the instruction shape (below)             */
+  SUBSPEC_PATH_MFMA16 = 3, /* MFMA path on 16x16x32 instructions (row tiles of 16) */
+  SUBSPEC_PATH_MFMA32 = 4  /* MFMA path on 32x32x16 instructions, always 128 rows
+                              (four row blocks of 32; rows past M are padding)   */
 };
 
 /* Launch configuration chosen for one qlinear call (host-side description). */
 typedef struct subspec_plan {
   int path;            /* SUBSPEC_PATH_GEMV or SUBSPEC_PATH_MFMA                  */
+  int mfma_rows;       /* MFMA path: 16 (16x16x32 bf16 instructions) or 32
+                          (32x32x16 bf16); 0 on the GEMV path.  The automatic
+                          choice takes 32 only for M > 64 and launches that either
+                          fill every CU with whole 128-column groups or split a K
+                          of at least 24576 (measured on the Qwen2.5 shapes)     */
   int rows;            /* rows computed per workgroup (M rounded up)              */
   int tiles_per_wave;  /* 16-column tiles each wavefront owns                     */
   int waves;           /* wavefronts per workgroup                                */
   int chunk_blocks;    /* 128-k blocks staged in LDS per step                     */
+  int ring_chunks;     /* MFMA path: chunks of weights in each wavefront's register
+                          ring (0 = the kernel's default; GEMV: ring stages)     */
   int col_groups;      /* column groups (waves * tiles_per_wave * 16 columns each) */
   int full_groups;     /* column groups [0, full_groups) run whole, one workgroup
                           each; the others are split along K                    */
@@ -151,7 +162,7 @@ int subspec_qpack_host(const uint8_t* codes, int bits, int N, int K, void* qweig
  *   zeros    device fp16 [K/group][N]
  *   y        device bf16 [M][N] row-major, fully overwritten
  * x and y must not overlap each other or the weights.  Uses the library's
- * per-device workspace when the plan splits K (see subspec_reserve); calls that
+ * per-device workspace (see subspec_reserve: the call may grow it); calls that
  * overlap in time on one device (different streams) must not share it, so
  * serialise them. */
 int subspec_qlinear(const void* x, const void* qweight, const void* scales,
@@ -159,7 +170,8 @@ int subspec_qlinear(const void* x, const void* qweight, const void* scales,
                     void* y, hipStream_t stream);
 
 /* subspec_qlinear with an explicit kernel path (SUBSPEC_PATH_*): for tests and
- * A/B measurements.  SUBSPEC_PATH_GEMV requires M <= 8. */
+ * A/B measurements.  SUBSPEC_PATH_GEMV requires M <= 8.  All paths compute the same
+ * function; they differ in the order of the fp32 additions only. */
 int subspec_qlinear_path(const void* x, const void* qweight, const void* scales,
                          const void* zeros, int bits, int group, int M, int N, int K,
                          void* y, int path, hipStream_t stream);
@@ -204,7 +216,8 @@ typedef struct subspec_graph subspec_graph;
 
 /* Capture subspec_stack_forward(projs, ...) on `stream` (which must not be the null
  * stream) into a graph and instantiate it.  The workspace the sequence needs is
- * reserved before capture.  The graph keeps the pointers of `projs` (not the array):
+ * reserved before capture; the graph keeps using that buffer, which stays allocated
+ * until the graph is destroyed even if later calls grow the workspace.  The graph keeps the pointers of `projs` (not the array):
  * replays read and write the same buffers. */
 int subspec_stack_capture(const subspec_proj* projs, int nproj, int bits, int group, int M,
                           hipStream_t stream, subspec_graph** graph);
@@ -212,7 +225,8 @@ int subspec_stack_capture(const subspec_proj* projs, int nproj, int bits, int gr
 /* Replay a captured sequence on `stream` (asynchronous). */
 int subspec_graph_launch(subspec_graph* graph, hipStream_t stream);
 
-/* Release a captured sequence (synchronous with respect to its replays). */
+/* Release a captured sequence (synchronises the device).  Destroying the device's
+ * last live graph frees the workspace buffers retired while graphs were alive. */
 int subspec_graph_destroy(subspec_graph* graph);
 
 /* Draft-tree expansion with probability sharpening (Sec. 4.2 "Constructing Deep
@@ -319,9 +333,28 @@ int subspec_prefetch_acquire(subspec_prefetch* pf, long long ticket, hipStream_t
                              void** dev_ptr);
 int subspec_prefetch_release(subspec_prefetch* pf, long long ticket, hipStream_t compute);
 
-/* Grow the calling device's workspace to at least `bytes` now (synchronous, may
- * call hipMalloc), so that later calls, e.g. under stream capture, need not. */
+/* The per-device workspace.  subspec_qlinear, subspec_tree_expand and
+ * subspec_tree_attention share one device buffer per device: its first 64 KiB are
+ * split-K completion counters (zero between calls), the rest is scratch for the call
+ * in flight.  A call that needs more than the buffer holds grows it: hipMalloc of a
+ * buffer at least twice as large, its counters zeroed on the call's stream, and a
+ * wait on that stream only (never on the whole device).  The old buffer is retired,
+ * not freed, because kernels queued on other streams or captured graphs
+ * (subspec_stack_capture) may still use it.  Retired buffers are freed by
+ * subspec_reserve while no captured graph is alive on the device, and when the
+ * device's last captured graph is destroyed; both synchronise the device first.  A
+ * call made after subspec_reserve(bytes) with a need of at most `bytes` neither
+ * allocates, frees nor synchronises.
+ *
+ * subspec_reserve: grow the calling device's workspace to at least `bytes` now
+ * (synchronous; may call hipMalloc) and free retired buffers as above, so that later
+ * calls, e.g. under stream capture, need not allocate. */
 int subspec_reserve(size_t bytes);
+
+/* Current state of the calling device's workspace: its size in bytes, the number of
+ * retired buffers still held, and how many buffers it has allocated so far.  Any
+ * output pointer may be null.  Host only; no GPU work. */
+int subspec_workspace_info(size_t* bytes, int* retired, unsigned long long* allocations);
 
 /* Description of the last failure on this thread ("" if none). */
 const char* subspec_last_error(void);

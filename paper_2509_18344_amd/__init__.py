@@ -10,6 +10,8 @@ from ._binding import (  # noqa: F401
     SUBSPEC_PATH_AUTO,
     SUBSPEC_PATH_GEMV,
     SUBSPEC_PATH_MFMA,
+    SUBSPEC_PATH_MFMA16,
+    SUBSPEC_PATH_MFMA32,
     SubspecError,
     library_path,
     load_library,
@@ -24,6 +26,7 @@ from ._binding import (  # noqa: F401
     subspec_quantize,
     subspec_quantize_hqq,
     subspec_reserve,
+    subspec_workspace_info,
     subspec_stack_forward,
     subspec_stack_capture,
     subspec_graph_launch,

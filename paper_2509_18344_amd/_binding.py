@@ -12,6 +12,8 @@ _LIB_NAME = "libsubspec.so"
 SUBSPEC_PATH_AUTO = 0
 SUBSPEC_PATH_GEMV = 1
 SUBSPEC_PATH_MFMA = 2
+SUBSPEC_PATH_MFMA16 = 3
+SUBSPEC_PATH_MFMA32 = 4
 
 _STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EHIP", -4: "ECAPTURE"}
 
@@ -24,9 +26,10 @@ class SubspecError(RuntimeError):
 
 
 class _Plan(ctypes.Structure):
-    _fields_ = [("path", ctypes.c_int), ("rows", ctypes.c_int), ("tiles_per_wave", ctypes.c_int),
+    _fields_ = [("path", ctypes.c_int), ("mfma_rows", ctypes.c_int), ("rows", ctypes.c_int),
+                ("tiles_per_wave", ctypes.c_int),
                 ("waves", ctypes.c_int),
-                ("chunk_blocks", ctypes.c_int), ("col_groups", ctypes.c_int),
+                ("chunk_blocks", ctypes.c_int), ("ring_chunks", ctypes.c_int), ("col_groups", ctypes.c_int),
                 ("full_groups", ctypes.c_int),
                 ("splits", ctypes.c_int), ("blocks_per_split", ctypes.c_int),
                 ("grid", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t)]
@@ -67,6 +70,8 @@ def load_library():
         "subspec_qlinear_plan": (I, [I, I, I, I, I, I, ctypes.POINTER(_Plan)]),
         "subspec_qdequant": (I, [P, P, P, I, I, I, I, P, P, P]),
         "subspec_reserve": (I, [S]),
+        "subspec_workspace_info": (I, [ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_int),
+                                       ctypes.POINTER(ctypes.c_ulonglong)]),
         "subspec_stack_forward": (I, [ctypes.POINTER(SubspecProj), I, I, I, I, P]),
         "subspec_stack_capture": (I, [ctypes.POINTER(SubspecProj), I, I, I, I, P,
                                       ctypes.POINTER(ctypes.c_void_p)]),
@@ -178,6 +183,14 @@ def subspec_qdequant(qweight, scales, zeros, bits, group, N, K, w_f32, w_bf16,
 
 def subspec_reserve(nbytes: int) -> int:
     return _check("subspec_reserve", load_library().subspec_reserve(nbytes))
+
+
+def subspec_workspace_info() -> dict:
+    """The calling device's workspace: bytes, retired buffers held, allocations so far."""
+    b, r, a = ctypes.c_size_t(), ctypes.c_int(), ctypes.c_ulonglong()
+    _check("subspec_workspace_info", load_library().subspec_workspace_info(
+        ctypes.byref(b), ctypes.byref(r), ctypes.byref(a)))
+    return {"bytes": int(b.value), "retired": int(r.value), "allocations": int(a.value)}
 
 
 def _projs(projs):

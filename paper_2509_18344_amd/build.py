@@ -3,13 +3,15 @@
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsubspec.so")
 HOST_SOURCES = ["api.cpp"]
-DEVICE_SOURCES = ["kernels_qlinear.hip", "kernels_prep.hip", "kernels_tree.hip", "kernels_attn.hip"]
+DEVICE_SOURCES = ["kernels_qlinear.hip", "kernels_qmma.hip", "kernels_qmma_b2.hip", "kernels_qmma_b3.hip",
+                  "kernels_qmma_b4.hip", "kernels_prep.hip", "kernels_tree.hip", "kernels_attn.hip"]
 OBJDIR = os.path.join(ROOT, "_build")
 
 HIPCC_FLAGS = [
@@ -41,15 +43,17 @@ def build(verbose: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     os.makedirs(OBJDIR, exist_ok=True)
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
-    objs = []
+    jobs = []
     for s in HOST_SOURCES:
         o = os.path.join(OBJDIR, s + ".o")
-        _run(["g++", *HOST_FLAGS, *inc, "-c", os.path.join(CSRC, s), "-o", o], verbose)
-        objs.append(o)
+        jobs.append((["g++", *HOST_FLAGS, *inc, "-c", os.path.join(CSRC, s), "-o", o], o))
     for s in DEVICE_SOURCES:
         o = os.path.join(OBJDIR, s + ".o")
-        _run([hipcc, *HIPCC_FLAGS, *inc, "-c", os.path.join(CSRC, s), "-o", o], verbose)
-        objs.append(o)
+        jobs.append(([hipcc, *HIPCC_FLAGS, *inc, "-c", os.path.join(CSRC, s), "-o", o], o))
+    # the translation units are independent: compile them side by side
+    with ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 1, 8)) as ex:
+        list(ex.map(lambda j: _run(j[0], verbose), jobs))
+    objs = [o for _, o in jobs]
     _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", *objs, "-o", LIB + ".tmp"], verbose)
     os.replace(LIB + ".tmp", LIB)
     return LIB

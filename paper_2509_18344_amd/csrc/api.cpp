@@ -83,6 +83,11 @@ struct Tuning {
   int fill_cus = 2;               // partial-sum cap still gives each CU this many workgroups
   int splits = 0;                 // 0 = choose per shape
   int partial_div = 2;            // split-K partial traffic may reach weight bytes / this
+  // Largest M the automatic MFMA plan keeps on 16x16x32 tiles (k_qgemm_mfma) in all
+  // cases; above it, k_qmma where it measured faster (see make_plan).
+  int mma16_max_m = 64;
+  int mma_nb = 0;                 // 32x32 kernel: 32-column blocks per wavefront; 0 = choose
+  int mma_shape = 0;              // automatic MFMA plans: 16 or 32 forces the tile shape
 };
 
 // Optional overrides for measurement sweeps: SUBSPEC_TUNE="gemv_max_m=4,target=512,...".
@@ -115,6 +120,9 @@ const Tuning& tuning() {
         else if (k == "fill_cus") r.fill_cus = v;
         else if (k == "splits") r.splits = v;
         else if (k == "partial_div") r.partial_div = v;
+        else if (k == "mma16_max_m") r.mma16_max_m = v;
+        else if (k == "mma_nb") r.mma_nb = v;
+        else if (k == "mma_shape") r.mma_shape = v;
       }
       pos = end + 1;
     }
@@ -138,6 +146,13 @@ int device_cus() {
   return cus;
 }
 
+// Bytes of the per-group sums of x the 32x32 kernel reads (fp32 [M][K/group]),
+// rounded up to 256.
+size_t xsum_bytes(const subspec::KernelChoice& c, int M, int K, int group) {
+  if (c.shape != 32) return 0;
+  return (static_cast<size_t>(M) * (K / group) * sizeof(float) + 255) & ~size_t(255);
+}
+
 int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* p,
               subspec::KernelChoice* kc) {
   int rc = check_bits_group(bits, group);
@@ -149,6 +164,19 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   if (path == SUBSPEC_PATH_AUTO) path = (M <= tu.gemv_max_m) ? SUBSPEC_PATH_GEMV : SUBSPEC_PATH_MFMA;
   const int KB = K / subspec::kTileK;
   const int n_tiles = N / subspec::kTileN;
+  // 32x32x16 tiles (k_qmma, 128 rows, 128 columns per workgroup) against 16x16x32
+  // (k_qgemm_mfma).  Measured on the Qwen2.5-7B/32B stacks at M = 96 and 128, k_qmma
+  // wins where its workgroups fill every CU without splitting K (gate|up: 7B 52.8
+  // against 66.0 us, 32B 3-bit 98.0 against 122.0 us at M = 96) and, one workgroup per
+  // CU with a four-chunk ring, on splits of a long K (32B down, K = 27648: 65.7
+  // against 68.2 us); on the short split launches (q|k|v, o; 7B down, K = 18944) the
+  // 16x16x32 kernel is faster (7B o at M = 128: 25.8 against 32.0 us).
+  const bool wide = (N + 127) / 128 >= device_cus();
+  const bool long_k = KB >= 192;
+  if (path == SUBSPEC_PATH_MFMA) {
+    const bool use32 = tu.mma_shape ? tu.mma_shape == 32 : M > tu.mma16_max_m && (wide || long_k);
+    path = use32 ? SUBSPEC_PATH_MFMA32 : SUBSPEC_PATH_MFMA16;
+  }
   subspec::KernelChoice c{};
   c.waves = 4;
   if (path == SUBSPEC_PATH_GEMV) {
@@ -161,8 +189,20 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     // use low enough for more resident waves; measured faster than deeper rings.
     c.chunk = tu.gemv_ch ? tu.gemv_ch : c.rows <= 2 ? 2 : 4;
     c.prefetch = tu.gemv_pf;
-  } else if (path == SUBSPEC_PATH_MFMA) {
+  } else if (path == SUBSPEC_PATH_MFMA32) {
+    // 32x32x16 matrix cores (k_qmma): four row blocks of 32, four wavefronts of one
+    // 32-column block each, one 128-k chunk per LDS stage.  The ring is two chunks
+    // deep (two workgroups per CU) when whole column groups fill the device, four
+    // deep (one workgroup per CU, more loads in flight each) when K is split.
     c.path = 2;
+    c.shape = 32;
+    c.rows = 128;
+    c.nt = 2 * (tu.mma_nb ? tu.mma_nb : 1);
+    c.chunk = 1;
+    c.prefetch = tu.mfma_pf ? tu.mfma_pf : wide ? 2 : 4;
+  } else if (path == SUBSPEC_PATH_MFMA16) {
+    c.path = 2;
+    c.shape = 16;
     const int mt = M <= 16 ? 1 : M <= 32 ? 2 : M <= 64 ? 4 : 8;
     c.rows = 16 * mt;
     // LDS holds two chunks of rows x (128*chunk) activations (at most 64 KB).  Short
@@ -174,7 +214,11 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   } else {
     return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
   }
-  if (!subspec::qlinear_variant_exists(c, bits, group))
+  auto variant_exists = [&](const subspec::KernelChoice& k) {
+    return k.shape == 32 ? subspec::qmma_variant_exists(k.rows / 32, k.nt / 2, k.prefetch, bits, group)
+                         : subspec::qlinear_variant_exists(k, bits, group);
+  };
+  if (!variant_exists(c))
     return fail(SUBSPEC_EUNSUPPORTED, "no kernel for path=%d rows=%d nt=%d chunk=%d waves=%d bits=%d group=%d",
                 c.path, c.rows, c.nt, c.chunk, c.waves, bits, group);
 
@@ -187,7 +231,8 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
       lds = subspec::gemv_lds_bytes(k.rows, std::min(K, subspec::gemv_max_kspan(k.rows, k.waves, group, cols)),
                                     group, cols);
     }
-    int per_cu = subspec::qlinear_resident_blocks(k, bits, group, lds);
+    int per_cu = k.shape == 32 ? subspec::qmma_resident_blocks(k.rows / 32, k.nt / 2, k.prefetch, bits, group)
+                               : subspec::qlinear_resident_blocks(k, bits, group, lds);
     if (per_cu <= 0) per_cu = 2;
     return per_cu * device_cus();
   };
@@ -204,7 +249,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   // M = 64: 36.7 against 38.4 us); at eight row tiles the two-tile variant fits one
   // wavefront per SIMD and loses.  Otherwise two tiles only pay when the one-tile
   // launch would need a second residency round.
-  if (c.path == 2 && !tu.mfma_nt) {
+  if (c.path == 2 && c.shape == 16 && !tu.mfma_nt) {
     subspec::KernelChoice c2 = c;
     c2.nt = 2;
     if (subspec::qlinear_variant_exists(c2, bits, group)) {
@@ -281,19 +326,35 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   const int blocks_per_split = chunks_per_split * c.chunk;
   splits = (KB + blocks_per_split - 1) / blocks_per_split;
   if (splits == 1) full_groups = 0;
-  p->path = path;
+  if (c.path == 1) {
+    // The clamps above (counter count, 32-bit partial offsets) can undo the GEMV
+    // minimum split count; a split that spans more of K than the kernel stages in LDS
+    // would read unstaged activations, so such shapes are refused.
+    const int span = subspec::gemv_max_kspan(c.rows, c.waves, group, cols_per_group);
+    const long long split_k = static_cast<long long>(splits == 1 ? KB : blocks_per_split) * subspec::kTileK;
+    if (std::min<long long>(split_k, K) > span)
+      return fail(SUBSPEC_EUNSUPPORTED,
+                  "GEMV path: M=%d N=%d K=%d needs splits of at most %d k, but the plan can only "
+                  "split %d ways (%d column groups)", M, N, K, span, splits, col_groups);
+  }
+  p->path = c.path == 1 ? SUBSPEC_PATH_GEMV : SUBSPEC_PATH_MFMA;
+  p->mfma_rows = c.path == 2 ? c.shape : 0;
   p->rows = c.rows;
   p->tiles_per_wave = c.nt;
   p->waves = c.waves;
   p->chunk_blocks = c.chunk;
+  p->ring_chunks = c.prefetch;
   p->col_groups = col_groups;
   p->full_groups = full_groups;
   p->splits = splits;
   p->blocks_per_split = blocks_per_split;
   p->grid = full_groups + (col_groups - full_groups) * splits;
+  // Workspace: split-K completion counters, then (32x32 kernel) the per-group sums of
+  // x, then the splits' fp32 partial sums.
   p->workspace_bytes = 0;
-  if (splits > 1)
-    p->workspace_bytes = subspec::kSplitCounterBytes + static_cast<size_t>(splits) * M * N * sizeof(float);
+  if (splits > 1 || c.shape == 32)
+    p->workspace_bytes = subspec::kSplitCounterBytes + xsum_bytes(c, M, K, group) +
+                         (splits > 1 ? static_cast<size_t>(splits) * M * N * sizeof(float) : 0);
   if (kc) *kc = c;
   return SUBSPEC_OK;
 }
@@ -303,6 +364,9 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
+  int graphs = 0;                // live captured graphs made on this device
+  std::vector<void*> retired;    // earlier buffers: queued kernels or graphs may still use them
+  unsigned long long allocations = 0;
 };
 std::mutex g_ws_mutex;
 std::vector<Workspace> g_ws;
@@ -313,15 +377,33 @@ int current_device(int* dev) {
   return SUBSPEC_OK;
 }
 
-// Returns the device's workspace, grown to `bytes` if needed.  Growth allocates
-// synchronously, so it is refused while `st` is being captured.
+Workspace& workspace_of(int dev) {  // caller holds g_ws_mutex
+  if (static_cast<int>(g_ws.size()) <= dev) g_ws.resize(dev + 1);
+  return g_ws[dev];
+}
+
+// Frees the retired buffers of `w`; the caller has synchronised the device.
+int free_retired(Workspace& w) {
+  int rc = SUBSPEC_OK;
+  for (void* p : w.retired) {
+    const hipError_t e = hipFree(p);
+    if (e != hipSuccess && rc == SUBSPEC_OK) rc = hip_fail(e, "hipFree(retired workspace)");
+  }
+  w.retired.clear();
+  return rc;
+}
+
+// Returns the device's workspace, grown to `bytes` if needed.  Growth allocates a new
+// buffer (at least twice the old size, so retired buffers total less than the live
+// one), zeroes its completion counters on `st` and waits for that stream only.  The
+// old buffer is retired, not freed: kernels queued on other streams and captured
+// graphs may still use it.  Growth is refused while `st` is being captured.
 int get_workspace(size_t bytes, hipStream_t st, void** out) {
   int dev = 0;
   int rc = current_device(&dev);
   if (rc) return rc;
   std::lock_guard<std::mutex> lock(g_ws_mutex);
-  if (static_cast<int>(g_ws.size()) <= dev) g_ws.resize(dev + 1);
-  Workspace& w = g_ws[dev];
+  Workspace& w = workspace_of(dev);
   if (w.bytes >= bytes) {
     *out = w.ptr;
     return SUBSPEC_OK;
@@ -334,28 +416,22 @@ int get_workspace(size_t bytes, hipStream_t st, void** out) {
       return fail(SUBSPEC_ECAPTURE, "workspace must grow to %zu bytes during stream capture; call "
                   "subspec_reserve() first", bytes);
   }
-  size_t nb = bytes < (size_t(1) << 20) ? (size_t(1) << 20) : bytes;
+  size_t nb = std::max({bytes, 2 * w.bytes, size_t(1) << 20});
   nb = (nb + 0xFFFFF) & ~size_t(0xFFFFF);
-  hipError_t e = hipDeviceSynchronize();  // the old buffer may still be in use
-  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
-  if (w.ptr) {
-    e = hipFree(w.ptr);
-    if (e != hipSuccess) return hip_fail(e, "hipFree(workspace)");
-    w.ptr = nullptr;
-    w.bytes = 0;
-  }
   void* p = nullptr;
-  e = hipMalloc(&p, nb);
+  hipError_t e = hipMalloc(&p, nb);
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
   // The split-K completion counters start at zero; every launch leaves them at zero.
-  e = hipMemset(p, 0, subspec::kSplitCounterBytes);
-  if (e == hipSuccess) e = hipDeviceSynchronize();
+  e = hipMemsetAsync(p, 0, subspec::kSplitCounterBytes, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) {
     (void)hipFree(p);
-    return hip_fail(e, "hipMemset(workspace counters)");
+    return hip_fail(e, "zeroing the workspace counters");
   }
+  if (w.ptr) w.retired.push_back(w.ptr);
   w.ptr = p;
   w.bytes = nb;
+  ++w.allocations;
   *out = p;
   return SUBSPEC_OK;
 }
@@ -422,14 +498,24 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
   a.splits = p.splits;
   a.blocks_per_split = p.blocks_per_split;
   a.span_blocks = p.full_groups > 0 ? a.KB : p.blocks_per_split;
-  if (p.splits > 1) {
+  if (p.workspace_bytes) {
     void* ws = nullptr;
     rc = get_workspace(p.workspace_bytes, st, &ws);
     if (rc) return rc;
-    a.cnt = static_cast<unsigned*>(ws);
-    a.ws = reinterpret_cast<float*>(static_cast<char*>(ws) + subspec::kSplitCounterBytes);
+    char* base = static_cast<char*>(ws);
+    const size_t xsb = xsum_bytes(kc, M, K, group);
+    a.cnt = reinterpret_cast<unsigned*>(base);
+    a.xsum = xsb ? reinterpret_cast<const float*>(base + subspec::kSplitCounterBytes) : nullptr;
+    a.ws = reinterpret_cast<float*>(base + subspec::kSplitCounterBytes + xsb);
   }
-  hipError_t e = subspec::launch_qlinear(kc, bits, group, a, p.grid, st);
+  hipError_t e = hipSuccess;
+  if (kc.shape == 32) {
+    e = subspec::launch_xsum(a.x, M, K, group, const_cast<float*>(a.xsum), st);
+    if (e == hipSuccess)
+      e = subspec::launch_qmma(kc.rows / 32, kc.nt / 2, kc.prefetch, bits, group, a, p.grid, st);
+  } else {
+    e = subspec::launch_qlinear(kc, bits, group, a, p.grid, st);
+  }
   if (e != hipSuccess) return hip_fail(e, "qlinear launch");
   return SUBSPEC_OK;
 }
@@ -536,6 +622,7 @@ int subspec_stack_forward(const subspec_proj* projs, int nproj, int bits, int gr
 struct subspec_graph {
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
+  int device = 0;  // its workspace buffers stay allocated while it lives
 };
 
 int subspec_stack_capture(const subspec_proj* projs, int nproj, int bits, int group, int M,
@@ -577,6 +664,13 @@ int subspec_stack_capture(const subspec_proj* projs, int nproj, int bits, int gr
   subspec_graph* g = new subspec_graph;
   g->graph = graph;
   g->exec = exec;
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  g->device = dev;
+  {
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    ++workspace_of(dev).graphs;
+  }
   *out = g;
   return SUBSPEC_OK;
 }
@@ -593,11 +687,19 @@ int subspec_graph_destroy(subspec_graph* g) {
   hipError_t e1 = hipDeviceSynchronize();
   hipError_t e2 = g->exec ? hipGraphExecDestroy(g->exec) : hipSuccess;
   hipError_t e3 = g->graph ? hipGraphDestroy(g->graph) : hipSuccess;
+  int rc = SUBSPEC_OK;
+  {
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    Workspace& w = workspace_of(g->device);
+    // The last graph of the device is gone and the device is idle: nothing can still
+    // reference a retired buffer.
+    if (--w.graphs == 0 && e1 == hipSuccess) rc = free_retired(w);
+  }
   delete g;
   if (e1 != hipSuccess) return hip_fail(e1, "hipDeviceSynchronize");
   if (e2 != hipSuccess) return hip_fail(e2, "hipGraphExecDestroy");
   if (e3 != hipSuccess) return hip_fail(e3, "hipGraphDestroy");
-  return SUBSPEC_OK;
+  return rc;
 }
 
 size_t subspec_tree_workspace_bytes(int R, int V, int k) {
@@ -672,7 +774,9 @@ int subspec_tree_attention(const void* q, void* k_cache, void* v_cache, const vo
     return fail(SUBSPEC_EUNSUPPORTED, "tree_attention: %d key ranges exceed %d", a.splits, subspec::kAttnMaxSplits);
   a.rows_pad = 16 * ((Hq / Hkv * M + 15) / 16);
   const size_t n = static_cast<size_t>(Hkv) * a.splits * a.rows_pad;
-  a.part_o = static_cast<float*>(ws);
+  // The first kSplitCounterBytes of the workspace are the split-K completion counters
+  // that qlinear and tree_expand rely on being zero: the partials go after them.
+  a.part_o = reinterpret_cast<float*>(static_cast<char*>(ws) + subspec::kSplitCounterBytes);
   a.part_ml = a.part_o + n * subspec::kAttnD;
   a.out = static_cast<uint16_t*>(out);
   const hipError_t e = subspec::launch_tree_attention(a, stream);
@@ -737,7 +841,29 @@ int subspec_tree_expand(const void* logits, const float* parent_logp, int R, int
 
 int subspec_reserve(size_t bytes) {
   void* p = nullptr;
-  return get_workspace(bytes, nullptr, &p);
+  int rc = get_workspace(bytes, nullptr, &p);
+  if (rc) return rc;
+  int dev = 0;
+  rc = current_device(&dev);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  Workspace& w = workspace_of(dev);
+  if (w.graphs > 0 || w.retired.empty()) return SUBSPEC_OK;
+  const hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  return free_retired(w);
+}
+
+int subspec_workspace_info(size_t* bytes, int* retired, unsigned long long* allocations) {
+  int dev = 0;
+  const int rc = current_device(&dev);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  const Workspace& w = workspace_of(dev);
+  if (bytes) *bytes = w.bytes;
+  if (retired) *retired = static_cast<int>(w.retired.size());
+  if (allocations) *allocations = w.allocations;
+  return SUBSPEC_OK;
 }
 
 const char* subspec_last_error(void) { return g_last_error.c_str(); }

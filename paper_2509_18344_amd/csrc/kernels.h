@@ -21,6 +21,7 @@ struct QArgs {
   uint16_t* y;            // bf16 [M][N]
   float* ws;              // fp32 [splits][M][N] partial sums (splits > 1)
   unsigned* cnt;          // per column group: workgroups done (zero between launches)
+  const float* xsum;      // k_qmma: fp32 [M][K/group] per-group sums of x (k_xsum)
   int M, N, K;
   int KB;                 // K / 128
   int n_tiles;            // N / 16
@@ -35,11 +36,12 @@ struct QArgs {
 
 struct KernelChoice {
   int path;    // 1 = GEMV, 2 = MFMA
-  int rows;    // GEMV: 1, 2, 4, 8; MFMA: 16 * m-tiles
+  int rows;    // GEMV: 1, 2, 4, 8; MFMA: 16 * m-tiles (shape 16) or 32 * m-blocks (shape 32)
   int nt;      // tiles per wavefront
   int chunk;   // 128-k blocks per LDS stage
   int waves;   // wavefronts per workgroup (4 or 8)
   int prefetch = 0;  // ring depth in chunks; 0 = the variant table's choice
+  int shape = 0;     // MFMA path: 16 = k_qgemm_mfma (16x16x32), 32 = k_qmma (32x32x16)
 };
 
 hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a,
@@ -52,6 +54,16 @@ int qlinear_resident_blocks(const KernelChoice& kc, int bits, int group, size_t 
 // dynamic LDS of one workgroup (cols = columns of the workgroup).
 int gemv_max_kspan(int rows, int waves, int group, int cols);
 size_t gemv_lds_bytes(int rows, int kspan, int group, int cols);
+
+// The 32x32x16 kernel (k_qmma): mb 32-row blocks, nb 32-column blocks per wavefront,
+// a ring of pf chunks; four wavefronts per workgroup.
+bool qmma_variant_exists(int mb, int nb, int pf, int bits, int group);
+int qmma_resident_blocks(int mb, int nb, int pf, int bits, int group);
+hipError_t launch_qmma(int mb, int nb, int pf, int bits, int group, const QArgs& a, int grid,
+                       hipStream_t st);
+// The sums of x over every group of k that k_qmma needs: out[m][g] = sum over the
+// group's k of x[m][k] (fp32), x bf16 [M][K].
+hipError_t launch_xsum(const uint16_t* x, int M, int K, int group, float* out, hipStream_t st);
 
 hipError_t launch_quantize(const float* w, int bits, int group, int N, int K, uint8_t* codes,
                            uint16_t* sc, uint16_t* zr, hipStream_t st);

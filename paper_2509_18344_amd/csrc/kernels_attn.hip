@@ -329,7 +329,8 @@ size_t attn_workspace_bytes(int M, int Hq, int Hkv, int P, int T) {
   attn_plan(M, Hq, Hkv, P, T, &splits, &tps);
   const int rows_pad = 16 * ((Hq / Hkv * M + 15) / 16);
   const size_t n = static_cast<size_t>(Hkv) * splits * rows_pad;
-  return n * kAttnD * sizeof(float) + n * 2 * sizeof(float);
+  // The partials follow the split-K completion counters at the workspace's start.
+  return kSplitCounterBytes + n * kAttnD * sizeof(float) + n * 2 * sizeof(float);
 }
 
 hipError_t launch_tree_attention(const AttnArgs& a, hipStream_t st) {

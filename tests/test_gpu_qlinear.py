@@ -73,10 +73,15 @@ def test_dequant_bit_exact(bits, group):
 SHAPES = [(512, 256), (528, 640), (1040, 1152)]  # tiles x blocks incl. ragged groups/chunks
 
 
+PATH_MS = {ss.SUBSPEC_PATH_GEMV: [1, 2, 3, 4, 5, 8],
+           ss.SUBSPEC_PATH_MFMA16: [1, 8, 16, 17, 33, 64, 100, 128],
+           ss.SUBSPEC_PATH_MFMA32: [1, 17, 64, 65, 100, 128]}
+
+
 @pytest.mark.parametrize("bits,group", [(4, 64), (4, 128), (3, 128), (3, 64), (2, 64), (2, 128)])
-@pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA])
+@pytest.mark.parametrize("path", list(PATH_MS))
 def test_qlinear_matches_oracle(bits, group, path):
-    ms = [1, 2, 3, 4, 5, 8] if path == ss.SUBSPEC_PATH_GEMV else [1, 8, 16, 17, 33, 64, 100, 128]
+    ms = PATH_MS[path]
     for (N, K) in SHAPES:
         w = _w(N, K, 300, N, K, bits, group)
         p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
@@ -91,10 +96,12 @@ def test_qlinear_matches_oracle(bits, group, path):
 @pytest.mark.parametrize("M,bits,group", [(1, 4, 128), (8, 4, 128), (40, 4, 128), (64, 4, 128),
                                           (2, 3, 128), (16, 3, 64), (5, 2, 64), (100, 2, 128)])
 def test_qlinear_balanced_tail_split(M, bits, group):
-    """More column groups than CUs (276 groups of 64 columns): the groups past a
-    multiple of the CU count run split along K while the others run whole; every
-    output is checked against the oracle."""
-    N, K = 16 * 4 * 276, 1024
+    """More column groups than CUs (276 column groups, of the width the plan uses at
+    this M): the groups past a multiple of the CU count run split along K while the
+    others run whole; every output is checked against the oracle."""
+    K = 1024
+    probe = ss.subspec_qlinear_plan(M, 16 * 4096, K, bits, group)
+    N = probe["waves"] * probe["tiles_per_wave"] * 16 * 276
     plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
     assert 0 < plan["full_groups"] < plan["col_groups"] and plan["splits"] > 1, plan
     w = _w(N, K, 310, M, bits, group)
@@ -108,7 +115,7 @@ def test_qlinear_balanced_tail_split(M, bits, group):
         assert_close(bf16_to_f64(y), y_ref, f"tail split M={M} bits={bits} g={group} plan={plan}")
 
 
-@pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA])
+@pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32])
 def test_qlinear_exact_integer_case(path):
     # s=1, z=0, codes in {0,1}, x in {-1,0,1}: every partial sum is a small integer,
     # so the GPU result must equal the oracle bit for bit.
@@ -131,7 +138,7 @@ def test_qlinear_deterministic():
     N, K = 1040, 1152
     w = _w(N, K, 400)
     p = device_projection(torch.from_numpy(w).to(DEV), 3, 128)
-    for path, M in [(ss.SUBSPEC_PATH_GEMV, 5), (ss.SUBSPEC_PATH_MFMA, 40)]:
+    for path, M in [(ss.SUBSPEC_PATH_GEMV, 5), (ss.SUBSPEC_PATH_MFMA16, 40), (ss.SUBSPEC_PATH_MFMA32, 100)]:
         x = synth.activations(M, K, 401, M).to(DEV)
         y1 = run_qlinear(p, x, path)
         y2 = run_qlinear(p, x, path)
@@ -158,7 +165,7 @@ def test_qlinear_does_not_touch_outside_y():
     x = synth.activations(M, K, 601).to(DEV)
     guard = torch.full((M * N + 2 * 4096,), -7, dtype=torch.int16, device=DEV)
     y = guard[4096:4096 + M * N].view(torch.bfloat16).view(M, N)
-    for path in (ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA):
+    for path in (ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32):
         ss.subspec_qlinear_path(x, p["qweight"], p["scales"], p["zeros"], 4, 64, M, N, K, y, path)
         torch.cuda.synchronize()
         assert torch.all(guard[:4096] == -7) and torch.all(guard[4096 + M * N:] == -7)

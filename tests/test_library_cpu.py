@@ -111,11 +111,13 @@ def test_plan_choices_are_consistent():
                     # once per CU
                     assert p["splits"] > 1 and fg % 256 == 0
                     assert (p["col_groups"] - fg) * p["splits"] <= 256
-                if p["splits"] == 1:
-                    assert p["workspace_bytes"] == 0
-                else:
-                    # completion counters (16384 x 4 bytes), then the fp32 partial sums
-                    assert p["workspace_bytes"] == 65536 + p["splits"] * M * N * 4
+                # completion counters (16384 x 4 bytes), the per-group sums of x the
+                # 32x32 kernel reads (fp32 [M][K/group], 256-byte aligned), then the
+                # splits' fp32 partial sums
+                xs = -(-M * (K // group) * 4 // 256) * 256 if p["mfma_rows"] == 32 else 0
+                partials = p["splits"] * M * N * 4 if p["splits"] > 1 else 0
+                expect = 65536 + xs + partials if (xs or partials) else 0
+                assert p["workspace_bytes"] == expect, (M, N, K, bits, group, p)
     # 592 column groups on 256 CUs: 512 whole, the last 80 split three ways
     p = ss.subspec_qlinear_plan(1, 37888, 3584, 4, 128)
     assert (p["col_groups"], p["full_groups"], p["splits"], p["grid"]) == (592, 512, 3, 752)
@@ -123,6 +125,42 @@ def test_plan_choices_are_consistent():
     assert ss.subspec_qlinear_plan(3, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_MFMA
     assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_GEMV)["path"] == ss.SUBSPEC_PATH_GEMV
     assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_MFMA)["path"] == ss.SUBSPEC_PATH_MFMA
+
+
+def test_mfma_tile_shape_choice():
+    """The automatic plan runs 32x32x16 tiles (128 rows) only above M = 64, on launches
+    that fill the 256 CUs with whole 128-column groups (two-chunk ring) or split a K of
+    at least 192 blocks (four-chunk ring); everything else stays on 16x16x32 tiles."""
+    def shape(M, N, K, bits=3, group=128, path=ss.SUBSPEC_PATH_AUTO):
+        p = ss.subspec_qlinear_plan(M, N, K, bits, group, path)
+        return p["mfma_rows"], p["rows"], p["ring_chunks"]
+    assert shape(128, 55296, 5120) == (32, 128, 2)   # 32B gate|up
+    assert shape(96, 37888, 3584, 4) == (32, 128, 2)  # 7B gate|up
+    assert shape(128, 5120, 27648) == (32, 128, 4)   # 32B down
+    assert shape(128, 7168, 5120)[0] == 16           # 32B q|k|v
+    assert shape(128, 3584, 18944, 4)[0] == 16       # 7B down
+    assert shape(64, 55296, 5120)[0] == 16
+    assert shape(17, 512, 256, path=ss.SUBSPEC_PATH_MFMA32) == (32, 128, 4)
+    assert shape(128, 55296, 5120, path=ss.SUBSPEC_PATH_MFMA16)[0] == 16
+    for path in (ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32):
+        assert ss.subspec_qlinear_plan(40, 512, 256, 4, 64, path)["path"] == ss.SUBSPEC_PATH_MFMA
+
+
+def test_gemv_plan_refuses_splits_longer_than_its_staging():
+    # At 8 rows a GEMV split stages at most 2048 k of x.  With more than 16384 column
+    # groups (N > 2^20) the plan cannot split K (one completion counter per group), so
+    # K = 2560 would leave 512 k unstaged: refused, never silently wrong.
+    N = (1 << 20) + 64
+    with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
+        ss.subspec_qlinear_plan(8, N, 2560, 4, 128, ss.SUBSPEC_PATH_GEMV)
+    assert "GEMV" in ss.subspec_last_error()
+    # the same shape with K inside one staged span, and the MFMA path, still plan
+    p = ss.subspec_qlinear_plan(8, N, 2048, 4, 128, ss.SUBSPEC_PATH_GEMV)
+    assert p["splits"] == 1
+    assert ss.subspec_qlinear_plan(8, N, 2560, 4, 128, ss.SUBSPEC_PATH_MFMA)["splits"] >= 1
+    # below the counter limit the plan splits K instead
+    p = ss.subspec_qlinear_plan(8, 65536, 8192, 4, 128, ss.SUBSPEC_PATH_GEMV)
+    assert p["splits"] * p["blocks_per_split"] * 128 >= 8192 and p["blocks_per_split"] * 128 <= 2048
 
 
 def test_qlinear_argument_errors_need_no_gpu():
@@ -189,7 +227,9 @@ def test_tree_attention_plan_and_errors_need_no_gpu():
         tiles = -(-(P + T + M) // 32)
         assert t >= 1 and (s - 1) * t < tiles <= s * t, (M, Hq, Hkv, P, T)
         rows_pad = 16 * -(-(Hq // Hkv * M) // 16)
-        assert ss.subspec_tree_attention_workspace_bytes(M, Hq, Hkv, P, T) == Hkv * s * rows_pad * (128 + 2) * 4
+        # the split-K completion counters (64 KiB) stay in front of the partials
+        assert ss.subspec_tree_attention_workspace_bytes(M, Hq, Hkv, P, T) == \
+            65536 + Hkv * s * rows_pad * (128 + 2) * 4
     for M, Hq, Hkv, P, T in [(6, 30, 4, 10, 0), (0, 28, 4, 10, 0), (10, 28, 4, 10, 0), (6, 28, 4, -1, 0),
                              (64, 1, 1, 0, 1100), (6, 4, 0, 10, 0)]:
         with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
