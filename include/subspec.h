@@ -169,6 +169,26 @@ int subspec_qlinear(const void* x, const void* qweight, const void* scales,
                     const void* zeros, int bits, int group, int M, int N, int K,
                     void* y, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops, harnesses that forbid hipMalloc): subspec_qlinear's contract, with
+ * the call's scratch (split-K completion counters, per-group sums of x, partial sums)
+ * taken from a fixed array of SUBSPEC_NOALLOC_SCRATCH_BYTES per device inside the
+ * library instead of the growable workspace.  The call never allocates or frees
+ * memory.  The plan is subspec_qlinear's, except that the split count is reduced where
+ * the partial sums would not fit: when subspec_qlinear_plan's workspace_bytes is at
+ * most SUBSPEC_NOALLOC_SCRATCH_BYTES the results are bit-identical to subspec_qlinear's,
+ * otherwise they differ in the order of fp32 additions only.  Shapes that need more
+ * scratch even unsplit return SUBSPEC_EUNSUPPORTED.  The first call on a device looks
+ * the array up and zeroes its counters on `stream` (waiting for that stream); that
+ * first call must not be captured (SUBSPEC_ECAPTURE), later calls may be.  All calls
+ * on one device share its array, which keeps the last call's contents: calls that
+ * overlap in time on one device (different streams, concurrent graph replays) race
+ * and must be serialised.  The array stays allocated until the process ends. */
+#define SUBSPEC_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int subspec_qlinear_noalloc(const void* x, const void* qweight, const void* scales,
+                            const void* zeros, int bits, int group, int M, int N, int K,
+                            void* y, hipStream_t stream);
+
 /* subspec_qlinear with an explicit kernel path (SUBSPEC_PATH_*): for tests and
  * A/B measurements.  SUBSPEC_PATH_GEMV requires M <= 8.  All paths compute the same
  * function; they differ in the order of the fp32 additions only. */

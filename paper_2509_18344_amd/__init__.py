@@ -19,6 +19,8 @@ from ._binding import (  # noqa: F401
     subspec_qdequant,
     subspec_qlinear,
     subspec_qlinear_path,
+    subspec_qlinear_noalloc,
+    SUBSPEC_NOALLOC_SCRATCH_BYTES,
     subspec_qlinear_plan,
     subspec_qpack,
     subspec_qpack_bytes,

@@ -14,6 +14,7 @@ SUBSPEC_PATH_GEMV = 1
 SUBSPEC_PATH_MFMA = 2
 SUBSPEC_PATH_MFMA16 = 3
 SUBSPEC_PATH_MFMA32 = 4
+SUBSPEC_NOALLOC_SCRATCH_BYTES = 32 << 20  # the fixed per-device scratch of subspec_qlinear_noalloc
 
 _STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EHIP", -4: "ECAPTURE"}
 
@@ -67,6 +68,7 @@ def load_library():
         "subspec_qpack_host": (I, [P, I, I, I, P]),
         "subspec_qlinear": (I, [P, P, P, P, I, I, I, I, I, P, P]),
         "subspec_qlinear_path": (I, [P, P, P, P, I, I, I, I, I, P, I, P]),
+        "subspec_qlinear_noalloc": (I, [P, P, P, P, I, I, I, I, I, P, P]),
         "subspec_qlinear_plan": (I, [I, I, I, I, I, I, ctypes.POINTER(_Plan)]),
         "subspec_qdequant": (I, [P, P, P, I, I, I, I, P, P, P]),
         "subspec_reserve": (I, [S]),
@@ -158,6 +160,11 @@ def subspec_qlinear(x, qweight, scales, zeros, bits, group, M, N, K, y, stream=N
     return _check("subspec_qlinear", load_library().subspec_qlinear(
         _ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), bits, group, M, N, K, _ptr(y),
         _stream(stream)))
+
+
+def subspec_qlinear_noalloc(x, qweight, scales, zeros, bits, group, M, N, K, y, stream=None) -> int:
+    return _check("subspec_qlinear_noalloc", load_library().subspec_qlinear_noalloc(
+        _ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), bits, group, M, N, K, _ptr(y), _stream(stream)))
 
 
 def subspec_qlinear_path(x, qweight, scales, zeros, bits, group, M, N, K, y, path,

@@ -11,7 +11,8 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsubspec.so")
 HOST_SOURCES = ["api.cpp"]
 DEVICE_SOURCES = ["kernels_qlinear.hip", "kernels_qmma.hip", "kernels_qmma_b2.hip", "kernels_qmma_b3.hip",
-                  "kernels_qmma_b4.hip", "kernels_prep.hip", "kernels_tree.hip", "kernels_attn.hip"]
+                  "kernels_qmma_b4.hip", "kernels_prep.hip", "kernels_tree.hip", "kernels_attn.hip",
+                  "noalloc.hip"]
 OBJDIR = os.path.join(ROOT, "_build")
 
 HIPCC_FLAGS = [

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdint>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -153,8 +154,11 @@ size_t xsum_bytes(const subspec::KernelChoice& c, int M, int K, int group) {
   return (static_cast<size_t>(M) * (K / group) * sizeof(float) + 255) & ~size_t(255);
 }
 
+// ws_cap bounds the workspace the plan may use (the allocation-free entry point's
+// fixed scratch array): the split count shrinks to fit, and a plan that cannot fit
+// even unsplit is refused.
 int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* p,
-              subspec::KernelChoice* kc) {
+              subspec::KernelChoice* kc, size_t ws_cap = SIZE_MAX) {
   int rc = check_bits_group(bits, group);
   if (rc) return rc;
   rc = check_tiles(N, K);
@@ -303,7 +307,16 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     return sp;
   };
   if (col_groups > subspec::kSplitCounters) splits = 1;
-  splits = fit_offsets(splits);
+  const size_t fixed_ws = subspec::kSplitCounterBytes + xsum_bytes(c, M, K, group);
+  auto fit_cap = [&](int sp) {
+    if (sp > 1 && ws_cap != SIZE_MAX) {
+      const size_t room = ws_cap > fixed_ws ? ws_cap - fixed_ws : 0;
+      const size_t most = room / (static_cast<size_t>(4) * M * N);
+      if (static_cast<size_t>(sp) > most) sp = static_cast<int>(std::max<size_t>(1, most));
+    }
+    return sp;
+  };
+  splits = fit_cap(fit_offsets(splits));
 
   // Balanced tail.  With col_groups = base * CUs + rem (base >= 1), whole column groups
   // alone leave rem CUs one group ahead of the rest (592 groups on 256 CUs: 80 CUs run
@@ -315,7 +328,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   if (splits == 1 && tu.tail && !tu.splits && col_groups <= subspec::kSplitCounters &&
       (c.path != 1 || K <= subspec::gemv_max_kspan(c.rows, c.waves, group, cols_per_group))) {
     const int base = col_groups / cus, rem = col_groups % cus;
-    const int ts = fit_offsets(std::min(rem ? cus / rem : 0, chunks));
+    const int ts = fit_cap(fit_offsets(std::min(rem ? cus / rem : 0, chunks)));
     if (base >= 1 && ts >= 2) {
       full_groups = base * cus;
       splits = ts;
@@ -355,6 +368,9 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   if (splits > 1 || c.shape == 32)
     p->workspace_bytes = subspec::kSplitCounterBytes + xsum_bytes(c, M, K, group) +
                          (splits > 1 ? static_cast<size_t>(splits) * M * N * sizeof(float) : 0);
+  if (p->workspace_bytes > ws_cap)
+    return fail(SUBSPEC_EUNSUPPORTED, "M=%d N=%d K=%d: needs %zu bytes of scratch even unsplit, above the "
+                "%zu available", M, N, K, p->workspace_bytes, ws_cap);
   if (kc) *kc = c;
   return SUBSPEC_OK;
 }
@@ -474,11 +490,14 @@ void pack_host(const uint8_t* codes, int N, int K, uint8_t* out) {
       }
 }
 
+// noalloc: take the scratch from the library's fixed per-device array (no allocation,
+// splits capped to its size) instead of the growable workspace.
 int qlinear_impl(const void* x, const void* qweight, const void* scales, const void* zeros,
-                 int bits, int group, int M, int N, int K, void* y, int path, hipStream_t st) {
+                 int bits, int group, int M, int N, int K, void* y, int path, hipStream_t st,
+                 bool noalloc = false) {
   subspec_plan p;
   subspec::KernelChoice kc;
-  int rc = make_plan(M, N, K, bits, group, path, &p, &kc);
+  int rc = make_plan(M, N, K, bits, group, path, &p, &kc, noalloc ? subspec::kNoAllocScratchBytes : SIZE_MAX);
   if (rc) return rc;
   if (!x || !qweight || !scales || !zeros || !y) return fail(SUBSPEC_EINVAL, "null pointer argument");
   if (!aligned16(x) || !aligned16(qweight) || !aligned16(scales) || !aligned16(zeros) || !aligned16(y))
@@ -500,8 +519,16 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
   a.span_blocks = p.full_groups > 0 ? a.KB : p.blocks_per_split;
   if (p.workspace_bytes) {
     void* ws = nullptr;
-    rc = get_workspace(p.workspace_bytes, st, &ws);
-    if (rc) return rc;
+    if (noalloc) {
+      const hipError_t e = subspec::noalloc_scratch(st, &ws);
+      if (e == hipErrorStreamCaptureUnsupported)
+        return fail(SUBSPEC_ECAPTURE, "subspec_qlinear_noalloc: the first call on a device sets up its scratch "
+                    "array and must not be captured");
+      if (e != hipSuccess) return hip_fail(e, "scratch array set-up");
+    } else {
+      rc = get_workspace(p.workspace_bytes, st, &ws);
+      if (rc) return rc;
+    }
     char* base = static_cast<char*>(ws);
     const size_t xsb = xsum_bytes(kc, M, K, group);
     a.cnt = reinterpret_cast<unsigned*>(base);
@@ -581,6 +608,11 @@ int subspec_qpack_host(const uint8_t* codes, int bits, int N, int K, void* qweig
 int subspec_qlinear(const void* x, const void* qweight, const void* scales, const void* zeros,
                     int bits, int group, int M, int N, int K, void* y, hipStream_t stream) {
   return qlinear_impl(x, qweight, scales, zeros, bits, group, M, N, K, y, SUBSPEC_PATH_AUTO, stream);
+}
+
+int subspec_qlinear_noalloc(const void* x, const void* qweight, const void* scales, const void* zeros,
+                            int bits, int group, int M, int N, int K, void* y, hipStream_t stream) {
+  return qlinear_impl(x, qweight, scales, zeros, bits, group, M, N, K, y, SUBSPEC_PATH_AUTO, stream, true);
 }
 
 int subspec_qlinear_path(const void* x, const void* qweight, const void* scales, const void* zeros,

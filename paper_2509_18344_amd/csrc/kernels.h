@@ -75,4 +75,13 @@ hipError_t launch_qdequant(const void* qw, const void* sc, const void* zr, int b
 constexpr int kSplitCounters = 16384;
 constexpr size_t kSplitCounterBytes = kSplitCounters * sizeof(unsigned);
 
+// The allocation-free qlinear entry point's scratch: one fixed array per device
+// (completion counters, x sums, partial sums), defined in noalloc.hip.
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;
+// Device address of the current device's scratch array, looked up on the first call
+// per device, which also zeroes the completion counters on `st` and waits for them.
+// That first call is refused (hipErrorStreamCaptureUnsupported) while `st` is being
+// captured; later calls do no GPU work and no allocation.
+hipError_t noalloc_scratch(hipStream_t st, void** out);
+
 }  // namespace subspec

@@ -163,6 +163,16 @@ def test_gemv_plan_refuses_splits_longer_than_its_staging():
     assert p["splits"] * p["blocks_per_split"] * 128 >= 8192 and p["blocks_per_split"] * 128 <= 2048
 
 
+def test_noalloc_refuses_shapes_beyond_its_fixed_scratch():
+    # 32x32 kernel at M = 128 over K = 4325376 with groups of 64: the sums of x alone
+    # (128 x 67584 fp32) exceed the 32 MiB array, so even an unsplit plan cannot fit;
+    # the call is refused while planning, before any GPU work
+    assert ss.SUBSPEC_NOALLOC_SCRATCH_BYTES == 32 << 20
+    with pytest.raises(ss.SubspecError, match="EUNSUPPORTED"):
+        ss.subspec_qlinear_noalloc(16, 16, 16, 16, 4, 64, 128, 256, 4325376, 16, stream=0)
+    assert "scratch" in ss.subspec_last_error()
+
+
 def test_qlinear_argument_errors_need_no_gpu():
     with pytest.raises(ss.SubspecError) as ei:
         ss.subspec_qlinear(None, 16, 16, 16, 4, 64, 1, 512, 256, 16, stream=0)
