@@ -1,40 +1,30 @@
 #!/usr/bin/env python3
 """Benchmark of the low-bit substitute-layer qlinear on one MI355X.
 
-Default workload: Qwen2.5-7B-shaped MLP projections (gate|up fused K=3584 N=37888,
-down K=18944 N=3584), 4-bit codes, groups of 128, fp16 scale/zero, bf16
-activations, at draft-tree batches M in {1, 8, 32, 64}.  One step = both launches
-at every M (8 launches).  Weights are rotated over enough distinct packed copies
-(>= 1 GB) that no launch finds its weights in the 256 MB last-level cache.
+Default (``--workload suite``): the headline is the Qwen2.5-32B-shaped 64-layer
+substitute stack (q|k|v, o, gate|up, down per layer; 3-bit codes, groups of 128,
+fp16 scale/zero) at draft-tree batches M in {1, 16, 64, 128}: one step = one pass
+of all 64 layers at every M, each M's pass captured as one HIP graph.  The same
+JSON line carries, under "configs", the tiny layer (K=256 N=512 4-bit g64 at M = 1
+and 4: per-call latency, weights cache-resident), the Qwen2.5-7B-shaped MLP
+projections (gate|up fused K=3584 N=37888, down K=18944 N=3584, 4-bit g128, M in
+{1, 8, 32, 64}, weights rotated over >= 1 GB of distinct copies), the 28-layer
+Qwen2.5-7B-shaped stack at M = 64, and the 64-layer 2-bit g64 32B-shaped stack
+with 1% outlier input channels at M = 128, each with its own roofline entry.
 
-The K timed steps run back to back on one stream between two HIP events (eager
-launches; ``--graph`` replays captured HIP graphs instead).  A second, separate
-pass brackets every launch with events to time each kernel on its own; the
-dominant kernel's roofline comes from that pass.  ``--workload
-qwen7b_stack|qwen32b_stack|qwen32b_2bit`` times whole substitute stacks (all
-layers, 4 launches per layer) captured as one HIP graph per M.
+Timing: W untimed steps, then K steps back to back between HIP events on the
+launch stream (ms_per_step = their total / K; step_ms = median, p10 and p90 of the
+per-step times).  Per launch: a HIP graph of that projection's launches over all
+layers (or weight copies) is replayed several times, one event pair per replay,
+so no host work sits between the timed calls; the dominant launch's roofline
+comes from that figure.  host_us_per_call is the host time of one eager
+subspec_qlinear call.  The GPU's clock levels are sampled (sysfs DPM tables) while
+the timed steps run, and a plain device copy's rate is given as context for the
+fraction of 8 TB/s.
 
 Prints one JSON line: effective weight GB/s (codes + scales + zeros bytes / time)
 of the whole step, the dominant kernel's roofline and the CPU oracle's rate on a
-bounded sample.
-
-``--summarize-pmc FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR`` turns four
-rocprofv3 ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` runs (of this script and of its
-``--copy-calibration-mb`` copy) into profiles/traffic.json (with ``--workload
-tree_expand``: profiles/traffic_tree.json), which later runs read for
-``roofline.traffic`` while that kernel family's sources are unchanged.
-
-``--workload tree_expand`` times the draft-tree expansion step instead (sharpened
-log-softmax of R x 152064 bf16 logits, parent scores, global top-6), and
-``--workload tree_attn`` one layer's tree attention over the shared KV cache
-(Qwen2.5-7B heads, 6 new tree tokens, 2048 committed positions, 282 earlier tree
-tokens: the last pass of a depth-48 tree).  Their traffic files are
-profiles/traffic_tree.json and profiles/traffic_attn.json.  ``--workload prefetch``
-times the target's verification pass over offloaded Qwen2.5-7B layers (bf16
-weights in pinned host memory, 289 tree tokens) with the cross-layer prefetcher,
-against copies alone, GEMMs alone and copy-then-compute.  ``--workload hqq`` times the
-quantizer with an HQQ-style optimised zero-point on one Qwen2.5-7B layer (4-bit,
-groups of 64), beside the min/max quantizer.
+bounded sample (one layer of the headline workload, host CPU model and BLAS named).
 """
 from __future__ import annotations
 
@@ -76,8 +66,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen7b_mlp",
-                    help="qwen7b_mlp (default), qwen7b_stack, qwen32b_stack, qwen32b_2bit, tiny, "
+    ap.add_argument("--workload", default="suite",
+                    help="suite (default: qwen32b_stack as the headline, then tiny, qwen7b_mlp, "
+                         "qwen7b_stack and qwen32b_2bit as extra entries), or one of qwen32b_stack, "
+                         "qwen7b_mlp, qwen7b_stack, qwen32b_2bit, tiny, "
                          "or tree_expand (the draft-tree expansion step; --ms gives its rows) "
                          "or tree_attn (one layer's tree attention over the shared KV cache) "
                          "or prefetch (verification pass over offloaded layers with cross-layer "
@@ -85,10 +77,14 @@ def parse():
     ap.add_argument("--ms", default=None, help="comma-separated M values (default: the workload's)")
     ap.add_argument("--rotate-gb", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-clocks", action="store_true",
+                    help="do not sample the GPU clock levels (sysfs) during the timed steps")
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 GEMV, 2 MFMA")
-    ap.add_argument("--graph", action="store_true",
-                    help="time HIP-graph replays of the step instead of eager launches")
-    ap.add_argument("--per-launch-reps", type=int, default=20)
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches of the projection workloads instead of HIP-graph "
+                         "replays (always eager with --path other than 0)")
+    ap.add_argument("--per-launch-reps", type=int, default=20,
+                    help="launches per timed burst of the tree and attention workloads")
     ap.add_argument("--json-out", default=None)
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (reference "
@@ -96,6 +92,10 @@ def parse():
     ap.add_argument("--summarize-trace", default=None, metavar="TRACE_DIR",
                     help="print a markdown table of a rocprofv3 --kernel-trace run's "
                          "library kernels per (kernel, grid) and exit")
+    ap.add_argument("--summarize-sq", nargs=3, default=None, metavar=("PASS_A_DIR", "PASS_B_DIR", "TRACE_DIR"),
+                    help="print a markdown table of the SQ counters (two --pmc passes of SQ_PASS_A "
+                         "and SQ_PASS_B) and kernel-trace durations of --workload's launches at "
+                         "--ms, and exit")
     ap.add_argument("--summarize-pmc", nargs=4, default=None,
                     metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"))
     return ap.parse_args()
@@ -196,9 +196,21 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, family="
                       "write_scale": out["calibration"]["write_scale"]}))
 
 
-def summarize_trace(d):
-    """Per (kernel, grid) dispatch durations of the library's kernels in a rocprofv3
-    kernel trace, as a markdown table (microseconds)."""
+def library_key(name, grid, wg):
+    """Dispatch key of a library kernel from its full name, grid and workgroup size
+    (work-items), the same key plan_key gives the qlinear kernels; None otherwise."""
+    m = re.search(r"(k_\w+)(<[^>]*>)?", name)
+    if not m or "subspec::" not in name:
+        return None
+    targs = [int(a) for a in m.group(2)[1:-1].split(",")] if m.group(2) else []
+    if m.group(1) in ("k_qgemv", "k_qgemm_mfma", "k_qmma"):
+        return dispatch_key(m.group(1), targs, grid, wg)
+    return f"{m.group(0)} grid={grid} wg={wg}"
+
+
+def trace_durations(d):
+    """Per dispatch key, the durations (us) of the library's kernels in a rocprofv3
+    kernel trace."""
     files = [os.path.join(dp, f) for dp, _, fs in os.walk(d) for f in fs
              if f.endswith("kernel_trace.csv")]
     if not files:
@@ -207,21 +219,72 @@ def summarize_trace(d):
     for fn in files:
         with open(fn) as f:
             for r in csv.DictReader(f):
-                m = re.search(r"(k_\w+)(<[^>]*>)?", r["Kernel_Name"])
-                if not m or "subspec::" not in r["Kernel_Name"]:
-                    continue
-                targs = [int(a) for a in m.group(2)[1:-1].split(",")] if m.group(2) else []
-                name = m.group(1)
-                if name in ("k_qgemv", "k_qgemm_mfma", "k_qmma"):
-                    key = dispatch_key(name, targs, int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
-                else:
-                    key = f"{m.group(0)} grid={r['Grid_Size_X']} wg={r['Workgroup_Size_X']}"
-                durs[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+                key = library_key(r["Kernel_Name"], int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
+                if key:
+                    durs[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    return durs
+
+
+def summarize_trace(d):
+    """Per (kernel, grid) dispatch durations of the library's kernels in a rocprofv3
+    kernel trace, as a markdown table (microseconds)."""
+    durs = trace_durations(d)
     print("| kernel (template args, grid and workgroup in work-items) | dispatches | avg us | median us | min us | max us |")
     print("|---|---|---|---|---|---|")
     for key, v in sorted(durs.items()):
         a = np.array(v)
         print(f"| `{key}` | {len(a)} | {a.mean():.2f} | {np.median(a):.2f} | {a.min():.2f} | {a.max():.2f} |")
+
+
+SQ_PASS_A = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
+             "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU")
+SQ_PASS_B = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA",
+             "SQ_INSTS_LDS", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS")
+SIMDS = 1024
+SCLK_GHZ = 2.4
+
+
+def summarize_sq(dir_a, dir_b, trace_dir, wl_key, ms):
+    """Markdown table of the SQ counters of every launch of a qlinear workload: two
+    rocprofv3 --pmc passes (SQ_PASS_A, SQ_PASS_B) and a kernel trace of the same
+    command.  Run where the counters were taken (the launch plans, hence the dispatch
+    keys, depend on the device)."""
+    import paper_2509_18344_amd as ss
+    from paper_2509_18344_amd.workloads import WORKLOADS, Proj, fused_layer
+    wl = WORKLOADS[wl_key]
+    if wl.key == "qwen7b_mlp":
+        projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
+    else:
+        projs = fused_layer(wl.projs) if wl.layers > 1 else wl.projs
+    labels = {}
+    for M in ms:
+        for p in projs:
+            plan = ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group)
+            labels.setdefault(plan_key(plan, wl.bits, wl.group), f"{p.name} M={M}")
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for d, names in ((dir_a, SQ_PASS_A), (dir_b, SQ_PASS_B)):
+        for c in names:
+            for name, grid, wg, v in _counter_rows(d, c):
+                key = library_key(name, grid, wg)
+                if key in labels:
+                    vals[key][c].append(v)
+    durs = trace_durations(trace_dir)
+    print("| launch | kernel | dispatches | waves | issuing % | waiting for issue % | of which LDS % | "
+          "waitcnt/barrier % | VALU / wave | MFMA / wave | LDS / wave | trace avg us | MFMA busy % |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+    for key, label in labels.items():
+        v = {c: float(np.mean(x)) for c, x in vals[key].items()}
+        if not all(c in v for c in SQ_PASS_A + SQ_PASS_B) or key not in durs:
+            continue
+        waves = v["SQ_WAVES"]
+        wc = v["SQ_WAVE_CYCLES"]
+        avg = float(np.mean(durs[key]))
+        busy = v["SQ_VALU_MFMA_BUSY_CYCLES"] / (avg * 1e-6 * SCLK_GHZ * 1e9 * SIMDS)
+        print(f"| {label} | `{key.split(' grid')[0]}` | {len(vals[key]['SQ_WAVES'])} | {int(waves)} | "
+              f"{100 * v['SQ_ACTIVE_INST_ANY'] / wc:.0f} | {100 * v['SQ_WAIT_INST_ANY'] / wc:.0f} | "
+              f"{100 * v['SQ_WAIT_INST_LDS'] / wc:.0f} | {100 * v['SQ_WAIT_ANY'] / wc:.0f} | "
+              f"{v['SQ_INSTS_VALU'] / waves:.0f} | {v['SQ_INSTS_MFMA'] / waves:.0f} | "
+              f"{v['SQ_INSTS_LDS'] / waves:.0f} | {avg:.1f} | {100 * busy:.1f} |")
 
 
 def measured_traffic(key: str, family: str = "qlinear"):
@@ -238,6 +301,103 @@ def measured_traffic(key: str, family: str = "qlinear"):
     return None if entry is None else entry.get("hbm_bytes_per_launch")
 
 
+# --- host and device context ------------------------------------------------------
+
+def host_info():
+    """The host CPU model (from /proc/cpuinfo) and the BLAS numpy uses (threadpoolctl)."""
+    info = {"cpu_model": None, "blas": None, "blas_threads": None,
+            "affinity_cpus": len(os.sched_getaffinity(0))}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    info["cpu_model"] = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if blas:
+            info["blas"] = f"{blas[0].get('internal_api')} {blas[0].get('version')}".strip()
+            info["blas_threads"] = max(int(i.get("num_threads", 1)) for i in blas)
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        pass
+    return info
+
+
+def _dpm_level(path):
+    """The current level of a sysfs DPM table (the line marked '*'), e.g. '2400Mhz'."""
+    try:
+        with open(path) as f:
+            for ln in f:
+                if ln.rstrip().endswith("*"):
+                    return ln.split(":", 1)[1].replace("*", "").strip()
+    except OSError:
+        pass
+    return None
+
+
+class ClockSampler:
+    """Samples the GPU's shader and memory clock levels from sysfs (pp_dpm_sclk /
+    pp_dpm_mclk of the first card that has them) every `period` seconds on a thread
+    while a timed region runs; no child process, no GPU call."""
+
+    def __init__(self, period=0.05, enabled=True):
+        import glob
+        import threading
+        cards = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")) if enabled else []
+        self.dev = os.path.dirname(cards[0]) if cards else None
+        self.period = period
+        self.samples = []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        while not self._stop.is_set():
+            self.samples.append((_dpm_level(os.path.join(self.dev, "pp_dpm_sclk")),
+                                 _dpm_level(os.path.join(self.dev, "pp_dpm_mclk"))))
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.dev:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self.dev:
+            self._stop.set()
+            self._thread.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        sclk = collections.Counter(a for a, _ in self.samples)
+        mclk = collections.Counter(b for _, b in self.samples)
+        return {"samples": len(self.samples), "sclk": dict(sclk.most_common()),
+                "mclk": dict(mclk.most_common()), "source": self.dev + "/pp_dpm_{sclk,mclk}"}
+
+
+def copy_rate(torch, stream, mib=2048, replays=5):
+    """Device-to-device copy rate of torch's copy kernel over `mib` MiB, counting
+    the bytes read plus the bytes written: context for the fraction of 8 TB/s."""
+    n = mib << 20
+    with torch.cuda.stream(stream):
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        src.fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(replays):
+            dst.copy_(src)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / replays
+    del src, dst
+    return {"torch_copy_GBs_read_plus_write": round(2 * n / (ms * 1e-3) / 1e9, 1), "MiB": mib}
+
+
 # --- CPU oracle baseline --------------------------------------------------------
 
 def cpu_baseline(wl, ms, min_seconds=10.0):
@@ -248,11 +408,8 @@ def cpu_baseline(wl, ms, min_seconds=10.0):
     import paper_2509_18344_amd as ss
     from paper_2509_18344_amd import synth
     from paper_2509_18344_amd.workloads import Proj, fused_layer, weight_bytes
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl missing
-        blas_threads = len(os.sched_getaffinity(0))
+    host = host_info()
+    threads = host["blas_threads"] or host["affinity_cpus"]
     if wl.key == "qwen7b_mlp":
         projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
     elif wl.layers > 1:
@@ -286,49 +443,16 @@ def cpu_baseline(wl, ms, min_seconds=10.0):
             break
     wb = steps * len(ms) * sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in projs)
     names = "+".join(f"{p.name}(K={p.K},N={p.N})" for p in projs)
-    return {"value": round(wb / dt / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
+    return {"value": round(wb / dt / 1e9, 4), "unit": "GB/s", "cores": int(threads),
             "kind": "oracle", "seconds": round(dt, 3),
+            "cpu_model": host["cpu_model"], "blas": host["blas"],
             "sample": f"{steps} pass(es) of {names} at M in {list(ms)}"
                       f"{' (one layer of the stack)' if wl.layers > 1 else ''}: unpack + fp64 "
-                      f"dequant (one thread) + fp64 BLAS matmul ({blas_threads} threads); "
+                      f"dequant (one thread) + fp64 BLAS matmul ({threads} threads); "
                       f"{wb / 1e6:.1f} MB of weights"}
 
 
 # --- GPU timing -------------------------------------------------------------------
-
-def per_launch_stats(torch, ss, wl, items, reps, stream):
-    """Time each (M, proj, argsets) eagerly between events, `reps` times, cycling
-    through its argument sets (distinct weight copies)."""
-    from paper_2509_18344_amd.workloads import weight_bytes
-    out = []
-    for (M, p, argsets) in items:
-        ev = []
-        for r in range(reps):
-            a = argsets[r % len(argsets)]
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            ss.subspec_qlinear(a["x"], a["qweight"], a["scales"], a["zeros"], wl.bits, wl.group,
-                               M, p.N, p.K, a["y"], stream)
-            e1.record(stream)
-            ev.append((e0, e1))
-        torch.cuda.synchronize()
-        t = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3  # us
-        plan = ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group)
-        wb = weight_bytes(p.N, p.K, wl.bits, wl.group)
-        ab = wb + 2 * M * p.K + 2 * M * p.N
-        flops = 2.0 * M * p.N * p.K
-        avg = float(t.mean())
-        out.append({"proj": p.name, "M": M, "N": p.N, "K": p.K, "path": plan["path"],
-                    "key": plan_key(plan, wl.bits, wl.group), "grid": plan["grid"], "splits": plan["splits"],
-                    "avg_us": round(avg, 2), "p10_us": round(float(np.percentile(t, 10)), 2),
-                    "p90_us": round(float(np.percentile(t, 90)), 2),
-                    "weight_GBs": round(wb / (avg * 1e-6) / 1e9, 1),
-                    "alg_GBs": round(ab / (avg * 1e-6) / 1e9, 1),
-                    "TFLOPs": round(flops / (avg * 1e-6) / 1e12, 2),
-                    "alg_bytes": ab, "flops": flops})
-    return out
-
 
 def timed(torch, stream, fn, warmup, steps):
     for s in range(warmup):
@@ -344,15 +468,108 @@ def timed(torch, stream, fn, warmup, steps):
     return t0.elapsed_time(t1)
 
 
+def timed_steps(torch, stream, fn, warmup, steps, clocks=True):
+    """`warmup` untimed steps, then `steps` steps back to back between events on
+    `stream` (one event after each step, nothing waits between them).  Returns the
+    total milliseconds, the per-step milliseconds and the clock levels sampled while
+    the timed steps ran."""
+    for s in range(warmup):
+        fn(s)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    with ClockSampler(enabled=clocks) as cs:
+        ev[0].record(stream)
+        for s in range(steps):
+            fn(warmup + s)
+            ev[s + 1].record(stream)
+        torch.cuda.synchronize()
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
+    return ev[0].elapsed_time(ev[-1]), per, cs.summary()
+
+
+def pct(a, q):
+    return round(float(np.percentile(a, q)), 4)
+
+
+def per_launch_graph(torch, ss, wl, M, p, argsets, stream, replays=7, min_launches=32):
+    """Per-call time of one projection without host work between calls: a HIP graph
+    of n back-to-back launches of it (cycling through `argsets`, i.e. distinct weight
+    copies or layers) is replayed `replays` times, each replay between two events on
+    the launch stream; a call's time is the replay's time / n (for the 32x32 kernel
+    this includes its x-sum pre-pass)."""
+    from paper_2509_18344_amd.workloads import weight_bytes
+    n = max(min_launches, len(argsets))
+    lst = [dict(argsets[i % len(argsets)], N=p.N, K=p.K) for i in range(n)]
+    g = ss.subspec_stack_capture(lst, wl.bits, wl.group, M, stream)
+    try:
+        ss.subspec_graph_launch(g, stream)  # untimed first replay
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(replays + 1)]
+        ev[0].record(stream)
+        for r in range(replays):
+            ss.subspec_graph_launch(g, stream)
+            ev[r + 1].record(stream)
+        torch.cuda.synchronize()
+        t = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(replays)]) * 1e3 / n  # us
+    finally:
+        ss.subspec_graph_destroy(g)
+    plan = ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group)
+    wb = weight_bytes(p.N, p.K, wl.bits, wl.group)
+    ab = wb + 2 * M * p.K + 2 * M * p.N
+    flops = 2.0 * M * p.N * p.K
+    med = float(np.median(t))
+    return {"proj": p.name, "M": M, "N": p.N, "K": p.K, "path": plan["path"],
+            "key": plan_key(plan, wl.bits, wl.group), "grid": plan["grid"], "splits": plan["splits"],
+            "median_us": round(med, 2), "p10_us": pct(t, 10), "p90_us": pct(t, 90),
+            "calls_per_replay": n, "replays": replays,
+            "weight_GBs": round(wb / (med * 1e-6) / 1e9, 1),
+            "alg_GBs": round(ab / (med * 1e-6) / 1e9, 1),
+            "TFLOPs": round(flops / (med * 1e-6) / 1e12, 2),
+            "alg_bytes": ab, "flops": flops}
+
+
+def host_us_per_call(ss, wl, M, p, a, stream, calls=200):
+    """Host time of one eager subspec_qlinear call (argument marshalling, the plan,
+    the launch), averaged over `calls` calls issued without waiting."""
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(calls):
+        ss.subspec_qlinear(a["x"], a["qweight"], a["scales"], a["zeros"], wl.bits, wl.group, M, p.N, p.K,
+                           a["y"], stream)
+    t1 = time.perf_counter()
+    torch.cuda.synchronize()
+    return {"us": round((t1 - t0) * 1e6 / calls, 2), "call": f"{p.name} M={M} N={p.N} K={p.K}"}
+
+
+def roofline_of(dom, family="qlinear"):
+    """Roofline entry of the dominant launch (bound by HBM or by bf16 MFMA,
+    whichever its arithmetic intensity puts it under)."""
+    ridge = (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9)
+    if dom["flops"] / dom["alg_bytes"] > ridge:
+        r = {"bound": "mfma", "achieved": dom["TFLOPs"], "peak": MFMA_BF16_PEAK_TFLOPS,
+             "unit": "TFLOP/s", "frac": round(dom["TFLOPs"] / MFMA_BF16_PEAK_TFLOPS, 4)}
+    else:
+        r = {"bound": "hbm", "achieved": dom["alg_GBs"], "peak": HBM_PEAK_GBS,
+             "unit": "GB/s", "frac": round(dom["alg_GBs"] / HBM_PEAK_GBS, 4)}
+    r.update({"traffic": measured_traffic(dom["key"], family),
+              "kernel": f"{dom['key']} ({dom['proj']} M={dom['M']} N={dom['N']} K={dom['K']})",
+              "avg_us": dom["median_us"], "alg_bytes_per_launch": dom["alg_bytes"],
+              "flops_per_launch": dom["flops"],
+              "kernel_source_sha256_16": kernel_source_hash(family)})
+    return r
+
+
 def run_projections(args, torch, ss, wl, ms, stream):
-    """Independent projections at several M; weights rotate over distinct copies."""
+    """Independent projections at several M; weights rotate over distinct copies so
+    that no launch finds its weights in the last-level cache (the tiny workload,
+    a latency measurement, keeps one copy)."""
     from paper_2509_18344_amd import prepare, synth
     from paper_2509_18344_amd.workloads import Proj, weight_bytes
     projs = wl.projs
     if wl.key == "qwen7b_mlp":  # gate|up share x: one fused launch, as in the layer plan
         projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
     per_copy = sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in projs)
-    copies = max(1, int(math.ceil(args.rotate_gb * 1e9 / per_copy)))
+    copies = 1 if wl.key == "tiny" else max(1, int(math.ceil(args.rotate_gb * 1e9 / per_copy)))
     weights = []
     for c in range(copies):
         wc = []
@@ -382,7 +599,8 @@ def run_projections(args, torch, ss, wl, ms, stream):
 
     graphs = []
     period = copies // math.gcd(copies, nl)
-    if args.graph:
+    use_graph = not args.eager and args.path == 0
+    if use_graph:
         for s in range(period):  # one graph per M (the API captures one M at a time)
             gs = []
             for M in ms:
@@ -391,7 +609,7 @@ def run_projections(args, torch, ss, wl, ms, stream):
             graphs.append(gs)
 
     def step(s):
-        if args.graph:
+        if use_graph:
             for g in graphs[s % period]:
                 ss.subspec_graph_launch(g, stream)
             return
@@ -401,23 +619,25 @@ def run_projections(args, torch, ss, wl, ms, stream):
                                     wl.group, launches[li][0], d["N"], d["K"], d["y"],
                                     args.path, stream)
 
-    total_ms = timed(torch, stream, step, args.warmup, args.steps)
+    total_ms, per_step, clocks = timed_steps(torch, stream, step, args.warmup, args.steps, not args.no_clocks)
     for gs in graphs:
         for g in gs:
             ss.subspec_graph_destroy(g)
-    items = []
+    per = []
     for (M, pi) in launches:
         x, y = acts[(M, pi)]
-        items.append((M, projs[pi], [{"x": x, "y": y, **{k: weights[c][pi][k] for k in
-                                                          ("qweight", "scales", "zeros")}}
-                                     for c in range(copies)]))
-    per = per_launch_stats(torch, ss, wl, items, max(args.per_launch_reps, copies), stream)
-    return {"total_ms": total_ms, "per_launch": per, "launches_per_step": nl, "copies": copies,
-            "rotation_GB": round(copies * per_copy / 1e9, 2),
+        argsets = [{"x": x, "y": y, **{k: weights[c][pi][k] for k in ("qweight", "scales", "zeros")}}
+                   for c in range(copies)]
+        per.append(per_launch_graph(torch, ss, wl, M, projs[pi], argsets, stream))
+    M0, p0 = launches[0][0], projs[launches[0][1]]
+    host = host_us_per_call(ss, wl, M0, p0, dict(proj_dict(0, 0)), stream)
+    return {"total_ms": total_ms, "per_step": per_step, "per_launch": per, "launches_per_step": nl,
+            "copies": copies, "rotation_GB": round(copies * per_copy / 1e9, 2),
             "step_bytes": sum(weight_bytes(projs[pi].N, projs[pi].K, wl.bits, wl.group)
                               for (_, pi) in launches),
             "step_flops": sum(2.0 * M * projs[pi].N * projs[pi].K for (M, pi) in launches),
-            "timing": "HIP graph replays" if args.graph else "eager launches"}
+            "timing": "HIP graph replays" if use_graph else "eager launches",
+            "host_us_per_call": host, "clocks": clocks}
 
 
 def run_stack(args, torch, ss, wl, ms, stream):
@@ -434,6 +654,9 @@ def run_stack(args, torch, ss, wl, ms, stream):
                        prepare.quantize_pack(ps[0], wl.bits, wl.group) for ps in parts])
         del w
     torch.cuda.synchronize()
+    # every plan's workspace up front: no growth between the captures below
+    ss.subspec_reserve(max(ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group)["workspace_bytes"]
+                           for M in ms for p in plan))
     xs, ys, graphs = {}, {}, []
     for M in ms:
         xs[M] = [[synth.activations(M, p.K, 21, l, li, outlier_frac=wl.outlier_frac).to("cuda")
@@ -449,21 +672,68 @@ def run_stack(args, torch, ss, wl, ms, stream):
         for g in graphs:
             ss.subspec_graph_launch(g, stream)
 
-    total_ms = timed(torch, stream, step, args.warmup, args.steps)
+    total_ms, per_step, clocks = timed_steps(torch, stream, step, args.warmup, args.steps, not args.no_clocks)
     for g in graphs:
         ss.subspec_graph_destroy(g)
     per = []
     for M in ms:
-        items = [(M, p, [{"x": xs[M][l][li], "y": ys[M][l][li],
-                          **{k: packed[l][li][k] for k in ("qweight", "scales", "zeros")}}
-                         for l in range(wl.layers)]) for li, p in enumerate(plan)]
-        per += per_launch_stats(torch, ss, wl, items, wl.layers, stream)
+        for li, p in enumerate(plan):
+            argsets = [{"x": xs[M][l][li], "y": ys[M][l][li],
+                        **{k: packed[l][li][k] for k in ("qweight", "scales", "zeros")}}
+                       for l in range(wl.layers)]
+            per.append(per_launch_graph(torch, ss, wl, M, p, argsets, stream))
+    # host cost of an eager call: the shortest launch of the stack (o at the smallest M)
+    M0 = min(ms)
+    a = {"x": xs[M0][0][1], "y": ys[M0][0][1], **{k: packed[0][1][k] for k in ("qweight", "scales", "zeros")}}
+    host = host_us_per_call(ss, wl, M0, plan[1], a, stream)
     layer_bytes = sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in plan)
-    return {"total_ms": total_ms, "per_launch": per, "launches_per_step": 4 * wl.layers * len(ms),
+    del packed, xs, ys
+    return {"total_ms": total_ms, "per_step": per_step, "per_launch": per,
+            "launches_per_step": 4 * wl.layers * len(ms),
             "copies": 1, "rotation_GB": round(layer_bytes * wl.layers / 1e9, 2),
             "step_bytes": layer_bytes * wl.layers * len(ms),
             "step_flops": sum(wl.layers * 2.0 * M * p.N * p.K for M in ms for p in plan),
-            "timing": "HIP graph replays"}
+            "timing": "HIP graph replays", "host_us_per_call": host, "clocks": clocks}
+
+
+def run_qlinear(args, torch, ss, key, ms=None):
+    """One qlinear workload: the step's rate, its spread, the per-launch table and
+    the dominant launch's roofline."""
+    from paper_2509_18344_amd.workloads import WORKLOADS
+    wl = WORKLOADS[key]
+    ms = ms or wl.ms
+    stream = torch.cuda.Stream()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        r = run_stack(args, torch, ss, wl, ms, stream) if wl.layers > 1 else \
+            run_projections(args, torch, ss, wl, ms, stream)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    ms_per_step = r["total_ms"] / args.steps
+    value = r["step_bytes"] / (ms_per_step * 1e-3) / 1e9
+    per = r["per_launch"]
+    # dominant launch: the largest share of the step's kernel time
+    dom = max(per, key=lambda d: d["median_us"])
+    return {
+        "value": round(value, 1), "unit": "GB/s", "ms_per_step": round(ms_per_step, 4),
+        "step_ms": {"median": pct(r["per_step"], 50), "p10": pct(r["per_step"], 10),
+                    "p90": pct(r["per_step"], 90)},
+        "config": {"workload": f"{key}: {wl.description}", "bits": wl.bits, "group": wl.group,
+                   "ms": list(ms), "layers": wl.layers, "launches_per_step": r["launches_per_step"],
+                   "weight_bytes_per_step": r["step_bytes"], "distinct_weight_copies": r["copies"],
+                   "rotation_GB": r["rotation_GB"], "timing": r["timing"],
+                   "hbm_fraction_of_8TBs": round(value / HBM_PEAK_GBS, 4),
+                   "TFLOPs": round(r["step_flops"] / (ms_per_step * 1e-3) / 1e12, 2)},
+        "roofline": roofline_of(dom),
+        "gpu_clocks_during_steps": r["clocks"],
+        "host_us_per_call": r["host_us_per_call"],
+        "per_launch": [{k: v for k, v in d.items() if k not in ("alg_bytes", "flops")} for d in per],
+        "wall_s": round(time.perf_counter() - t0, 2),
+    }
+
+
+HEADLINE = "qwen32b_stack"
+EXTRA_CONFIGS = ("tiny", "qwen7b_mlp", "qwen7b_stack", "qwen32b_2bit")
 
 
 def main():
@@ -474,13 +744,18 @@ def main():
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
         return
+    if args.summarize_sq:
+        from paper_2509_18344_amd.workloads import WORKLOADS
+        key = HEADLINE if args.workload == "suite" else args.workload
+        ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else WORKLOADS[key].ms
+        summarize_sq(*args.summarize_sq, key, ms)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the library has no "
               "multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2509_18344_amd as ss
-    from paper_2509_18344_amd.workloads import WORKLOADS
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -507,63 +782,44 @@ def main():
     if args.workload == "hqq":
         run_hqq(args, torch, ss)
         return
-    wl = WORKLOADS[args.workload]
-    ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else wl.ms
-    stream = torch.cuda.Stream()
-    t_setup = time.perf_counter()
-    with torch.cuda.stream(stream):
-        if wl.layers > 1:
-            r = run_stack(args, torch, ss, wl, ms, stream)
-        else:
-            r = run_projections(args, torch, ss, wl, ms, stream)
-    wall_s = time.perf_counter() - t_setup
-
-    ms_per_step = r["total_ms"] / args.steps
-    value = r["step_bytes"] / (ms_per_step * 1e-3) / 1e9
-    per = r["per_launch"]
-    # dominant kernel: the launch with the largest share of the step's kernel time
-    dom = max(per, key=lambda d: d["avg_us"])
-    ridge = (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9)
-    if dom["flops"] / dom["alg_bytes"] > ridge:
-        roofline = {"bound": "mfma", "achieved": dom["TFLOPs"], "peak": MFMA_BF16_PEAK_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(dom["TFLOPs"] / MFMA_BF16_PEAK_TFLOPS, 4)}
-    else:
-        roofline = {"bound": "hbm", "achieved": dom["alg_GBs"], "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s", "frac": round(dom["alg_GBs"] / HBM_PEAK_GBS, 4)}
-    roofline.update({"traffic": measured_traffic(dom["key"]),
-                     "kernel": f"{dom['key']} ({dom['proj']} M={dom['M']} N={dom['N']} K={dom['K']})",
-                     "avg_us": dom["avg_us"], "alg_bytes_per_launch": dom["alg_bytes"],
-                     "flops_per_launch": dom["flops"],
-                     "kernel_source_sha256_16": kernel_source_hash()})
-
+    suite = args.workload == "suite"
+    key = HEADLINE if suite else args.workload
+    ms = tuple(int(m) for m in args.ms.split(",")) if args.ms else None
+    t_all = time.perf_counter()
+    head = run_qlinear(args, torch, ss, key, ms)
+    extras = {}
+    if suite:
+        for k in EXTRA_CONFIGS:
+            extras[k] = run_qlinear(args, torch, ss, k)
     out = {
         "metric": "effective weight GB/s and % HBM roofline of low-bit qlinear at draft-tree M",
-        "value": round(value, 1),
+        "value": head["value"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic: N(0,0.02) fp32 weights min/max-quantized on the GPU, N(0,1) bf16 "
                 "activations, seeded",
-        "config": {"workload": wl.description, "bits": wl.bits, "group": wl.group,
-                   "ms": list(ms), "layers": wl.layers,
-                   "launches_per_step": r["launches_per_step"],
-                   "weight_bytes_per_step": r["step_bytes"],
-                   "distinct_weight_copies": r["copies"], "rotation_GB": r["rotation_GB"],
-                   "timing": r["timing"],
-                   "hbm_fraction_of_8TBs": round(value / HBM_PEAK_GBS, 4),
-                   "TFLOPs": round(r["step_flops"] / (ms_per_step * 1e-3) / 1e12, 2)},
-        "roofline": roofline,
-        "per_launch": [{k: v for k, v in d.items() if k not in ("alg_bytes", "flops")} for d in per],
-        "wall_s": round(wall_s, 2),
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "step_ms": head["step_ms"],
+        "gpu_clocks_during_steps": head["gpu_clocks_during_steps"],
+        "host_us_per_call": head["host_us_per_call"],
+        "per_launch": head["per_launch"],
     }
+    if suite:
+        out["configs"] = extras
+    out["hbm_context"] = copy_rate(torch, torch.cuda.Stream())
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, ms)
+        from paper_2509_18344_amd.workloads import WORKLOADS
+        wl = WORKLOADS[key]
+        out["cpu_baseline"] = cpu_baseline(wl, ms or wl.ms)
+    out["wall_s"] = round(time.perf_counter() - t_all, 2)
     line = json.dumps(out)
     if args.json_out:
         with open(args.json_out, "w") as f:
