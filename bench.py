@@ -8,12 +8,14 @@ of all 64 layers at every M, each M's pass captured as one HIP graph.  The same
 JSON line carries, under "configs", the tiny layer (K=256 N=512 4-bit g64 at M = 1
 and 4: per-call latency, weights cache-resident), the Qwen2.5-7B-shaped MLP
 projections (gate|up fused K=3584 N=37888, down K=18944 N=3584, 4-bit g128, M in
-{1, 8, 32, 64}, weights rotated over >= 1 GB of distinct copies), the 28-layer
+{1, 8, 32, 64}, weights rotated over >= 1 GB of distinct copies), the same at the
+small draft batches M in {2, 4, 6, 8}, the 28-layer
 Qwen2.5-7B-shaped stack at M = 64, and the 64-layer 2-bit g64 32B-shaped stack
 with 1% outlier input channels at M = 128, each with its own roofline entry.
 
-Timing: W untimed steps, then K steps back to back between HIP events on the
-launch stream (ms_per_step = their total / K; step_ms = median, p10 and p90 of the
+Timing: untimed steps of the same work for half a second (the shader clock ramps up
+from idle over a few hundred ms), W untimed warm-up steps, then K steps back to back
+between HIP events on the launch stream (ms_per_step = their total / K; step_ms = median, p10 and p90 of the
 per-step times).  Per launch: a HIP graph of that projection's launches over all
 layers (or weight copies) is replayed several times, one event pair per replay,
 so no host work sits between the timed calls; the dominant launch's roofline
@@ -68,8 +70,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="suite",
                     help="suite (default: qwen32b_stack as the headline, then tiny, qwen7b_mlp, "
-                         "qwen7b_stack and qwen32b_2bit as extra entries), or one of qwen32b_stack, "
-                         "qwen7b_mlp, qwen7b_stack, qwen32b_2bit, tiny, "
+                         "qwen7b_mlp_draft, qwen7b_stack and qwen32b_2bit as extra entries), or one "
+                         "of those, "
                          "or tree_expand (the draft-tree expansion step; --ms gives its rows) "
                          "or tree_attn (one layer's tree attention over the shared KV cache) "
                          "or prefetch (verification pass over offloaded layers with cross-layer "
@@ -252,7 +254,7 @@ def summarize_sq(dir_a, dir_b, trace_dir, wl_key, ms):
     import paper_2509_18344_amd as ss
     from paper_2509_18344_amd.workloads import WORKLOADS, Proj, fused_layer
     wl = WORKLOADS[wl_key]
-    if wl.key == "qwen7b_mlp":
+    if wl.key.startswith("qwen7b_mlp"):
         projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
     else:
         projs = fused_layer(wl.projs) if wl.layers > 1 else wl.projs
@@ -260,7 +262,10 @@ def summarize_sq(dir_a, dir_b, trace_dir, wl_key, ms):
     for M in ms:
         for p in projs:
             plan = ss.subspec_qlinear_plan(M, p.N, p.K, wl.bits, wl.group)
-            labels.setdefault(plan_key(plan, wl.bits, wl.group), f"{p.name} M={M}")
+            key = plan_key(plan, wl.bits, wl.group)
+            name, msk = labels.get(key, (p.name, []))
+            labels[key] = (name, msk + [M])
+    labels = {k: f"{n} M={','.join(str(m) for m in msk)}" for k, (n, msk) in labels.items()}
     vals = collections.defaultdict(lambda: collections.defaultdict(list))
     for d, names in ((dir_a, SQ_PASS_A), (dir_b, SQ_PASS_B)):
         for c in names:
@@ -410,7 +415,7 @@ def cpu_baseline(wl, ms, min_seconds=10.0):
     from paper_2509_18344_amd.workloads import Proj, fused_layer, weight_bytes
     host = host_info()
     threads = host["blas_threads"] or host["affinity_cpus"]
-    if wl.key == "qwen7b_mlp":
+    if wl.key.startswith("qwen7b_mlp"):
         projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
     elif wl.layers > 1:
         projs = fused_layer(wl.projs)
@@ -468,11 +473,19 @@ def timed(torch, stream, fn, warmup, steps):
     return t0.elapsed_time(t1)
 
 
+SPIN_UP_S = 0.5  # the shader clock takes a few hundred ms to ramp from idle
+
+
 def timed_steps(torch, stream, fn, warmup, steps, clocks=True):
-    """`warmup` untimed steps, then `steps` steps back to back between events on
-    `stream` (one event after each step, nothing waits between them).  Returns the
-    total milliseconds, the per-step milliseconds and the clock levels sampled while
-    the timed steps ran."""
+    """Spin-up (untimed steps of the same work for SPIN_UP_S seconds, so the clock is
+    at its working level), `warmup` untimed steps, then `steps` steps back to back
+    between events on `stream` (one event after each step, nothing waits between
+    them).  Returns the total milliseconds, the per-step milliseconds and the clock
+    levels sampled while the timed steps ran."""
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < SPIN_UP_S:
+        fn(0)
+        torch.cuda.synchronize()
     for s in range(warmup):
         fn(s)
     torch.cuda.synchronize()
@@ -566,7 +579,7 @@ def run_projections(args, torch, ss, wl, ms, stream):
     from paper_2509_18344_amd import prepare, synth
     from paper_2509_18344_amd.workloads import Proj, weight_bytes
     projs = wl.projs
-    if wl.key == "qwen7b_mlp":  # gate|up share x: one fused launch, as in the layer plan
+    if wl.key.startswith("qwen7b_mlp"):  # gate|up share x: one fused launch, as in the layer plan
         projs = (Proj("gate_up", 3584, 2 * 18944), Proj("down", 18944, 3584))
     per_copy = sum(weight_bytes(p.N, p.K, wl.bits, wl.group) for p in projs)
     copies = 1 if wl.key == "tiny" else max(1, int(math.ceil(args.rotate_gb * 1e9 / per_copy)))
@@ -733,7 +746,7 @@ def run_qlinear(args, torch, ss, key, ms=None):
 
 
 HEADLINE = "qwen32b_stack"
-EXTRA_CONFIGS = ("tiny", "qwen7b_mlp", "qwen7b_stack", "qwen32b_2bit")
+EXTRA_CONFIGS = ("tiny", "qwen7b_mlp", "qwen7b_mlp_draft", "qwen7b_stack", "qwen32b_2bit")
 
 
 def main():

@@ -95,7 +95,6 @@ struct MmaBody {
   static constexpr int SPG = 8 / GPC;         // 16-k steps per group
   static constexpr int XCH = ROWS * 16;       // 16-byte pieces per chunk buffer
   static constexpr int DMA = ROWS / 16;      // x copy loads per wavefront per chunk
-  static constexpr bool kPrefetchA = MB <= 2;
 
   // One ring slot: the chunk's two slices per column block and the fp16 scale and
   // zero-point of the lane's column for each of the chunk's groups.
@@ -159,11 +158,11 @@ struct MmaBody {
                                                static_cast<uint32_t>(kb) * (kTileK * 2), 0, 0);
   }
 
-  // One chunk (x buffer X, ring slot wc).  Up to two row blocks the A fragments of
-  // the next step are read before the current step's MFMAs, so the LDS latency runs
-  // under them; with four row blocks the 16 registers that takes would push the kernel
-  // past two wavefronts per SIMD, and the other wavefront on the SIMD covers the
-  // latency instead.  cneg[gi][nb] receives -s*(128+z) of the chunk's groups.
+  // One chunk (x buffer X, ring slot wc).  The A fragments of the next step are read
+  // before the current step's MFMAs, so the LDS latency runs under them (16 more
+  // registers at four row blocks, still within two wavefronts per SIMD once the sums
+  // of x come from the pre-pass).  cneg[gi][nb] receives -s*(128+z) of the chunk's
+  // groups.
   static __device__ __forceinline__ void compute(const W& wc, const u32x4_t* X, int lane, const Lanes& ln,
                                                  f32x16_t (&tot)[MB][NB], float (&cneg)[GPC][NB]) {
     const int r32 = lane & 31, hi = lane >> 5;
@@ -182,12 +181,7 @@ struct MmaBody {
         constexpr int SS = decltype(ssc)::value;
         constexpr int S = gi * SPG + SS;  // 16-k step within the chunk
         bf16x8_t An[MB];
-        if constexpr (!kPrefetchA) {
-          if constexpr (S > 0) {
-#pragma unroll
-            for (int i = 0; i < MB; ++i) A[i] = read_a(i, 2 * S + hi);
-          }
-        } else if constexpr (S + 1 < 8) {
+        if constexpr (S + 1 < 8) {
 #pragma unroll
           for (int i = 0; i < MB; ++i) An[i] = read_a(i, 2 * (S + 1) + hi);
         }
@@ -199,7 +193,7 @@ struct MmaBody {
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
             acc[i][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i], B[nb], SS == 0 ? zero : acc[i][nb], 0, 0, 0);
-        if constexpr (kPrefetchA && S + 1 < 8) {
+        if constexpr (S + 1 < 8) {
 #pragma unroll
           for (int i = 0; i < MB; ++i) A[i] = An[i];
         }
@@ -271,7 +265,9 @@ __device__ __forceinline__ void chunk_barrier(const u32x4_t* next, uint32_t& tou
 // earlier; the only weight load issued before that copy and not yet needed is the one
 // for chunk c + 1 itself, so every weight load has XB - 1 chunks to arrive.
 template <int BITS, int GROUP, int MB, int NB, int XB>
-__global__ __launch_bounds__(kMmaWaves * kWave) __attribute__((amdgpu_waves_per_eu(2)))
+// Two workgroups per CU (two wavefronts per SIMD) fit the LDS of a two-chunk ring; a
+// deeper ring takes one workgroup per CU and may use the SIMD's whole register file.
+__global__ __launch_bounds__(kMmaWaves * kWave) __attribute__((amdgpu_waves_per_eu(XB <= 2 ? 2 : 1)))
 void k_qmma(QArgs a) {
   static_assert(XB % 2 == 0 && XB >= 2 && XB <= 6, "chunk parity (pairs of 128-k groups) follows the ring slot");
   using Body = MmaBody<BITS, GROUP, MB, NB>;

@@ -51,6 +51,10 @@ WORKLOADS = {
     "qwen7b_mlp": Workload("qwen7b_mlp", "Qwen2.5-7B-shaped MLP projections, 4-bit g128",
                            (Proj("gate", 3584, 18944), Proj("up", 3584, 18944),
                             Proj("down", 18944, 3584)), 4, 128, (1, 8, 32, 64)),
+    "qwen7b_mlp_draft": Workload("qwen7b_mlp_draft", "Qwen2.5-7B-shaped MLP projections, 4-bit g128, "
+                                 "at small draft batches (Sec. 5.1 draws k = 6 leaves per pass)",
+                                 (Proj("gate", 3584, 18944), Proj("up", 3584, 18944),
+                                  Proj("down", 18944, 3584)), 4, 128, (2, 4, 6, 8)),
     "qwen7b_stack": Workload("qwen7b_stack", "Qwen2.5-7B-shaped 28-layer substitute stack, "
                              "4-bit g128", QWEN7B, 4, 128, (64,), layers=28, fused=True),
     "qwen32b_stack": Workload("qwen32b_stack", "Qwen2.5-32B-shaped 64-layer substitute stack, "

@@ -1,6 +1,7 @@
 """GPU tests of the per-layer launch plan (q|k|v, o, gate|up, down per decoder layer)
-and of its HIP-graph capture, at small shapes in full and at the Qwen2.5-7B/32B stack
-shapes on sampled output columns, against the fp64 oracle."""
+and of its HIP-graph capture against the fp64 oracle: small shapes in full, and the
+Qwen2.5-7B/32B stacks at their full sizes, every output of the first and the last
+layer's launches (the whole stack runs as captured graphs)."""
 import numpy as np
 import pytest
 
@@ -21,7 +22,8 @@ TINY = (Proj("q", 256, 256), Proj("k", 256, 64), Proj("v", 256, 64), Proj("o", 2
 
 def _build(projs, layers, bits, group, cfg, keep_layers, sample):
     """Pack `layers` decoder layers (fused plan).  For the layers in keep_layers, keep
-    the fp32 rows (output columns) listed by sample(N) of every fused launch."""
+    the fp32 rows (output columns) listed by sample(N) of every fused launch (all of
+    them when sample is None)."""
     plan = fused_layer(projs)
     packed, kept = [], {}
     for l in range(layers):
@@ -32,8 +34,11 @@ def _build(projs, layers, bits, group, cfg, keep_layers, sample):
             wl = torch.cat(parts, 0) if len(parts) > 1 else parts[0]
             layer.append(prepare.quantize_pack(wl, bits, group))
             if l in keep_layers:
-                cols = sample(plan[li].N)
-                kept[(l, li)] = (cols, wl[cols].cpu().numpy())
+                if sample is None:
+                    kept[(l, li)] = (None, wl.cpu().numpy())
+                else:
+                    cols = sample(plan[li].N)
+                    kept[(l, li)] = (cols, wl[torch.as_tensor(cols, device=wl.device)].cpu().numpy())
             del wl
         packed.append(layer)
         del w
@@ -100,9 +105,27 @@ def _sample_cols(n):
     return np.unique(np.concatenate([base, [15, 16, n - 16, n - 1]]))
 
 
+def _check_every_output(w, bits, group, x_bits, y_gpu, what, block=1024):
+    """Every output column of one launch against the oracle: the fp32 weights w [N][K]
+    are quantized by the oracle in blocks of `block` columns (quantization is per
+    column, so a block's codes are the full matrix's), and each block's outputs are
+    compared for every M.  x_bits: {M: bf16 bits [M][K]}; y_gpu: {M: float64 [M][N]}."""
+    N = w.shape[0]
+    for n0 in range(0, N, block):
+        n1 = min(N, n0 + block)
+        q, s16, z16 = oracle.quantize_minmax(w[n0:n1], bits, group)
+        for M, xb in x_bits.items():
+            assert_close(y_gpu[M][:, n0:n1], oracle.qlinear_ref(xb, q, s16, z16, group),
+                         f"{what} M={M} columns {n0}:{n1}")
+
+
 def _run_stack_graph(wl, cfg, Ms, keep):
+    """Run the whole stack as one captured graph per M; compare every output of the
+    launches of the layers in `keep` with the oracle."""
     layers = wl.layers
-    plan, packed, kept = _build(wl.projs, layers, wl.bits, wl.group, cfg, keep, _sample_cols)
+    plan, packed, kept = _build(wl.projs, layers, wl.bits, wl.group, cfg, keep, None)
+    x_bits = {key: {} for key in kept}
+    y_gpu = {key: {} for key in kept}
     for M in Ms:
         xs, ys = _acts(plan, layers, M, cfg, wl.outlier_frac)
         xs_dev = [[x.to(DEV) for x in row] for row in xs]
@@ -115,10 +138,15 @@ def _run_stack_graph(wl, cfg, Ms, keep):
             side.synchronize()
         finally:
             ss.subspec_graph_destroy(g)
-        _check_sampled(kept, xs, ys, wl.bits, wl.group, f"{wl.key} M={M}")
-        del xs_dev, ys
+        for (l, li) in kept:
+            x_bits[(l, li)][M] = synth.bf16_bits(xs[l][li])
+            y_gpu[(l, li)][M] = bf16_to_f64(ys[l][li])
+        del xs_dev, ys, launches
     del packed
     torch.cuda.empty_cache()
+    for (l, li), (_, w) in sorted(kept.items()):
+        _check_every_output(w, wl.bits, wl.group, x_bits[(l, li)], y_gpu[(l, li)],
+                            f"{wl.key} layer={l} launch={plan[li].name}")
 
 
 def test_qwen7b_stack_28_layers_m64():
@@ -133,25 +161,27 @@ def test_qwen32b_stack_3bit():
 
 def test_qwen32b_stack_2bit_outliers_m128():
     wl = WORKLOADS["qwen32b_2bit"]
-    _run_stack_graph(wl, 5, [128], {0, 37, wl.layers - 1})
+    _run_stack_graph(wl, 5, [128], {0, wl.layers - 1})
 
 
-@pytest.mark.parametrize("M", [1, 8, 32, 64])
-def test_qwen7b_mlp_projections(M):
-    """gate|up (K=3584, N=37888) and down (K=18944, N=3584), 4-bit g128."""
+def test_qwen7b_mlp_projections():
+    """gate|up (K=3584, N=37888) and down (K=18944, N=3584), 4-bit g128, at
+    M in {1, 8, 32, 64}: every output against the oracle."""
     for li, (N, K) in enumerate([(37888, 3584), (3584, 18944)]):
         w = synth.weights_torch(N, K, 2, li)
         p = prepare.quantize_pack(w, 4, 128)
+        x_bits, y_gpu = {}, {}
+        for M in (1, 8, 32, 64):
+            x = synth.activations(M, K, 2, 100 + li, M)
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+            ss.subspec_qlinear(x.to(DEV), p["qweight"], p["scales"], p["zeros"], 4, 128, M, N, K, y)
+            x_bits[M] = synth.bf16_bits(x)
+            y_gpu[M] = bf16_to_f64(y)
+        w_host = w.cpu().numpy()
         cols = _sample_cols(N)
-        wrows = w[torch.as_tensor(cols, device=DEV)].cpu().numpy()
-        del w
-        x = synth.activations(M, K, 2, 100 + li, M)
-        y = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
-        ss.subspec_qlinear(x.to(DEV), p["qweight"], p["scales"], p["zeros"], 4, 128, M, N, K, y)
-        q, s16, z16 = oracle.quantize_minmax(wrows, 4, 128)
-        y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, 128)
-        assert_close(bf16_to_f64(y[:, torch.as_tensor(cols, device=DEV)]), y_ref,
-                     f"qwen7b mlp N={N} K={K} M={M}")
         # the quantizer on these columns is the oracle's, bit for bit
+        _, s16, _ = oracle.quantize_minmax(w_host[cols], 4, 128)
         assert np.array_equal(p["scales"][:, torch.as_tensor(cols, device=DEV)].cpu().numpy()
                               .view(np.uint16), s16.view(np.uint16))
+        del w, p
+        _check_every_output(w_host, 4, 128, x_bits, y_gpu, f"qwen7b mlp N={N} K={K}")

@@ -121,8 +121,9 @@ def test_plan_choices_are_consistent():
     # 592 column groups on 256 CUs: 512 whole, the last 80 split three ways
     p = ss.subspec_qlinear_plan(1, 37888, 3584, 4, 128)
     assert (p["col_groups"], p["full_groups"], p["splits"], p["grid"]) == (592, 512, 3, 752)
-    assert ss.subspec_qlinear_plan(2, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_GEMV
-    assert ss.subspec_qlinear_plan(3, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_MFMA
+    # automatic plan: GEMV only for one row (measured crossover), MFMA from M = 2
+    assert ss.subspec_qlinear_plan(1, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_GEMV
+    assert ss.subspec_qlinear_plan(2, 512, 256, 4, 64)["path"] == ss.SUBSPEC_PATH_MFMA
     assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_GEMV)["path"] == ss.SUBSPEC_PATH_GEMV
     assert ss.subspec_qlinear_plan(8, 512, 256, 4, 64, ss.SUBSPEC_PATH_MFMA)["path"] == ss.SUBSPEC_PATH_MFMA
 
