@@ -110,8 +110,10 @@ typedef struct subspec_plan {
   int blocks_per_split;/* 128-k blocks per split                                  */
   int grid;            /* total workgroups =
                           full_groups + (col_groups - full_groups) * splits      */
-  size_t workspace_bytes; /* device scratch needed when splits > 1: 64 KiB of
-                             completion counters + the splits' fp32 partial sums */
+  size_t workspace_bytes; /* device scratch the call uses: 64 KiB of completion
+                             counters, the 32x32 kernel's per-group sums of x, and
+                             the fp32 partial sums of split column groups (0 when
+                             none of these is needed) */
 } subspec_plan;
 
 /* Bytes of the packed code buffer for an N x K projection.  0 on bad arguments. */
