@@ -126,7 +126,8 @@ def plan_key(plan, bits, group) -> str:
         targs = (bits, group, plan["rows"], plan["tiles_per_wave"], plan["chunk_blocks"], plan["waves"])
     elif plan["mfma_rows"] == 32:
         family = "k_qmma"
-        targs = (bits, group, plan["rows"] // 32, plan["tiles_per_wave"] // 2, plan["ring_chunks"])
+        targs = (bits, group, plan["rows"] // 32, plan["tiles_per_wave"] // 2, plan["ring_chunks"],
+                 plan["waves"])
     else:
         family = "k_qgemm_mfma"
         targs = (bits, group, plan["rows"] // 16, plan["tiles_per_wave"], plan["chunk_blocks"], plan["waves"])

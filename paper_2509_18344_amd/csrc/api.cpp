@@ -92,6 +92,7 @@ struct Tuning {
   int mma16_max_m = 64;
   int mma_nb = 0;                 // 32x32 kernel: 32-column blocks per wavefront; 0 = choose
   int mma_shape = 0;              // automatic MFMA plans: 16 or 32 forces the tile shape
+  int mma_waves = 0;              // 32x32 kernel: wavefronts per workgroup (4 or 8); 0 = choose
 };
 
 // Optional overrides for measurement sweeps: SUBSPEC_TUNE="gemv_max_m=4,target=512,...".
@@ -127,6 +128,7 @@ const Tuning& tuning() {
         else if (k == "mma16_max_m") r.mma16_max_m = v;
         else if (k == "mma_nb") r.mma_nb = v;
         else if (k == "mma_shape") r.mma_shape = v;
+        else if (k == "mma_waves") r.mma_waves = v;
       }
       pos = end + 1;
     }
@@ -184,7 +186,8 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     const bool use32 = tu.mma_shape ? tu.mma_shape == 32 : M > tu.mma16_max_m && (wide || long_k);
     path = use32 ? SUBSPEC_PATH_MFMA32 : SUBSPEC_PATH_MFMA16;
   }
-  subspec::KernelChoice c{};
+  subspec::KernelChoice c{}, c8{};
+  bool use8 = false;  // 32x32 kernel: the eight-wavefront variant (c8) where it exists
   c.waves = 4;
   if (path == SUBSPEC_PATH_GEMV) {
     if (M > kGemvMaxRows) return fail(SUBSPEC_EUNSUPPORTED, "GEMV path needs M <= 8 (M=%d)", M);
@@ -207,6 +210,17 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c.nt = 2 * (tu.mma_nb ? tu.mma_nb : 1);
     c.chunk = 1;
     c.prefetch = tu.mfma_pf ? tu.mfma_pf : wide ? 2 : 4;
+    // Eight wavefronts of one 32-column block each share one x ring four chunks deep
+    // (one workgroup of 256 columns per CU): each wavefront then has three chunks of
+    // weights in flight instead of one.  Taken where 256-column groups still cover
+    // three quarters of the CUs and K is not split (32B gate|up, N = 55296, M = 128:
+    // 90.9 against 98.0 us at 3 bits, 97.1 against 103.1 at 2 bits; slower on the 7B
+    // gate|up's 148 groups and on the split 32B down projection).
+    const bool wide8 = (N + 255) / 256 * 4 >= 3 * device_cus();
+    c8 = c;
+    c8.waves = 8;
+    c8.prefetch = tu.mfma_pf ? tu.mfma_pf : 4;
+    use8 = tu.mma_waves == 8 || (!tu.mma_waves && wide8 && !long_k);
   } else if (path == SUBSPEC_PATH_MFMA16) {
     c.path = 2;
     c.shape = 16;
@@ -222,9 +236,10 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
   }
   auto variant_exists = [&](const subspec::KernelChoice& k) {
-    return k.shape == 32 ? subspec::qmma_variant_exists(k.rows / 32, k.nt / 2, k.prefetch, bits, group)
+    return k.shape == 32 ? subspec::qmma_variant_exists(k.waves, k.rows / 32, k.nt / 2, k.prefetch, bits, group)
                          : subspec::qlinear_variant_exists(k, bits, group);
   };
+  if (use8 && (tu.mma_waves == 8 || variant_exists(c8))) c = c8;
   if (!variant_exists(c))
     return fail(SUBSPEC_EUNSUPPORTED, "no kernel for path=%d rows=%d nt=%d chunk=%d waves=%d bits=%d group=%d",
                 c.path, c.rows, c.nt, c.chunk, c.waves, bits, group);
@@ -238,7 +253,8 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
       lds = subspec::gemv_lds_bytes(k.rows, std::min(K, subspec::gemv_max_kspan(k.rows, k.waves, group, cols)),
                                     group, cols);
     }
-    int per_cu = k.shape == 32 ? subspec::qmma_resident_blocks(k.rows / 32, k.nt / 2, k.prefetch, bits, group)
+    int per_cu = k.shape == 32 ? subspec::qmma_resident_blocks(k.waves, k.rows / 32, k.nt / 2, k.prefetch, bits,
+                                                               group)
                                : subspec::qlinear_resident_blocks(k, bits, group, lds);
     if (per_cu <= 0) per_cu = 2;
     return per_cu * device_cus();
@@ -590,7 +606,7 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
   if (kc.shape == 32) {
     e = subspec::launch_xsum(a.x, M, K, group, const_cast<float*>(a.xsum), st);
     if (e == hipSuccess)
-      e = subspec::launch_qmma(kc.rows / 32, kc.nt / 2, kc.prefetch, bits, group, a, p.grid, st);
+      e = subspec::launch_qmma(kc.waves, kc.rows / 32, kc.nt / 2, kc.prefetch, bits, group, a, p.grid, st);
   } else {
     e = subspec::launch_qlinear(kc, bits, group, a, p.grid, st);
   }

@@ -55,11 +55,11 @@ int qlinear_resident_blocks(const KernelChoice& kc, int bits, int group, size_t 
 int gemv_max_kspan(int rows, int waves, int group, int cols);
 size_t gemv_lds_bytes(int rows, int kspan, int group, int cols);
 
-// The 32x32x16 kernel (k_qmma): mb 32-row blocks, nb 32-column blocks per wavefront,
-// a ring of pf chunks; four wavefronts per workgroup.
-bool qmma_variant_exists(int mb, int nb, int pf, int bits, int group);
-int qmma_resident_blocks(int mb, int nb, int pf, int bits, int group);
-hipError_t launch_qmma(int mb, int nb, int pf, int bits, int group, const QArgs& a, int grid,
+// The 32x32x16 kernel (k_qmma): `waves` wavefronts per workgroup (4 or 8), mb 32-row
+// blocks, nb 32-column blocks per wavefront, a ring of pf chunks.
+bool qmma_variant_exists(int waves, int mb, int nb, int pf, int bits, int group);
+int qmma_resident_blocks(int waves, int mb, int nb, int pf, int bits, int group);
+hipError_t launch_qmma(int waves, int mb, int nb, int pf, int bits, int group, const QArgs& a, int grid,
                        hipStream_t st);
 // The sums of x over every group of k that k_qmma needs: out[m][g] = sum over the
 // group's k of x[m][k] (fp32), x bf16 [M][K].

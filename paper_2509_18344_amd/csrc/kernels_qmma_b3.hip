@@ -3,12 +3,15 @@
 
 namespace subspec {
 
-#define SUBSPEC_QMMA(G, MB, NB, PF) {MB, NB, PF, 3, G, qmma::k_qmma<3, G, MB, NB, PF>}
+#define SUBSPEC_QMMA(G, MB, NB, PF, W) {MB, NB, PF, W, 3, G, qmma::k_qmma<3, G, MB, NB, PF, W>}
 
-// Four row blocks (M = 65..128), the ring two chunks deep (two workgroups per CU) or
-// four (one workgroup per CU, for launches split along a long K).
+// Four row blocks (M = 65..128).  Four wavefronts with the ring two chunks deep (two
+// workgroups per CU) or four (one workgroup per CU, for launches split along a long K);
+// eight wavefronts (256 columns, one workgroup per CU) with the ring four chunks deep.
+// (The eight-wavefront build spills registers with groups of 64.)
 static const MmaVariant kVariants[] = {
-    SUBSPEC_QMMA(128, 4, 1, 2), SUBSPEC_QMMA(128, 4, 1, 4), SUBSPEC_QMMA(64, 4, 1, 2), SUBSPEC_QMMA(64, 4, 1, 4),
+    SUBSPEC_QMMA(128, 4, 1, 2, 4), SUBSPEC_QMMA(128, 4, 1, 4, 4), SUBSPEC_QMMA(128, 4, 1, 4, 8),
+    SUBSPEC_QMMA(64, 4, 1, 2, 4),  SUBSPEC_QMMA(64, 4, 1, 4, 4),
 };
 
 const MmaVariant* qmma_variants_b3(int* n) {

@@ -3,12 +3,14 @@
 
 namespace subspec {
 
-#define SUBSPEC_QMMA(G, MB, NB, PF) {MB, NB, PF, 4, G, qmma::k_qmma<4, G, MB, NB, PF>}
+#define SUBSPEC_QMMA(G, MB, NB, PF, W) {MB, NB, PF, W, 4, G, qmma::k_qmma<4, G, MB, NB, PF, W>}
 
-// Four row blocks (M = 65..128), the ring two chunks deep (two workgroups per CU) or
-// four (one workgroup per CU, for launches split along a long K).
+// Four row blocks (M = 65..128), four wavefronts, the ring two chunks deep (two
+// workgroups per CU) or four (one workgroup per CU, for launches split along a long K).
+// (The eight-wavefront build spills registers at four bits.)
 static const MmaVariant kVariants[] = {
-    SUBSPEC_QMMA(128, 4, 1, 2), SUBSPEC_QMMA(128, 4, 1, 4), SUBSPEC_QMMA(64, 4, 1, 2), SUBSPEC_QMMA(64, 4, 1, 4),
+    SUBSPEC_QMMA(128, 4, 1, 2, 4), SUBSPEC_QMMA(128, 4, 1, 4, 4), SUBSPEC_QMMA(64, 4, 1, 2, 4),
+    SUBSPEC_QMMA(64, 4, 1, 4, 4),
 };
 
 const MmaVariant* qmma_variants_b4(int* n) {

@@ -37,7 +37,6 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 
 namespace qmma {
 
-constexpr int kMmaWaves = 4;
 typedef __attribute__((address_space(3))) void* LdsPtr;
 
 // LDS of one workgroup: two chunks of x, each [rows][16 pieces of 8 k] with the
@@ -88,13 +87,14 @@ __device__ __forceinline__ Slice<BITS> load_slice_s(__amdgpu_buffer_rsrc_t r, ui
   return s;
 }
 
-template <int BITS, int GROUP, int MB, int NB>
+template <int BITS, int GROUP, int MB, int NB, int WAVES>
 struct MmaBody {
   static constexpr int ROWS = 32 * MB;
   static constexpr int GPC = kTileK / GROUP;  // groups per 128-k chunk
   static constexpr int SPG = 8 / GPC;         // 16-k steps per group
   static constexpr int XCH = ROWS * 16;       // 16-byte pieces per chunk buffer
-  static constexpr int DMA = ROWS / 16;      // x copy loads per wavefront per chunk
+  static constexpr int DMA = ROWS / (4 * WAVES);  // x copy loads per wavefront per chunk
+  static_assert(DMA * 4 * WAVES == ROWS, "each copy load fills four rows");
 
   // One ring slot: the chunk's two slices per column block and the fp16 scale and
   // zero-point of the lane's column for each of the chunk's groups.
@@ -145,16 +145,16 @@ struct MmaBody {
   // into an LDS buffer: each load instruction fills 1 KB (four consecutive rows) with
   // 16 bytes per lane in lane order, so lane l writes position l % 16 of its row and
   // fetches the piece that the swizzle puts there.  Load j of wavefront w covers rows
-  // 4w + 16j + (0..3): a lane keeps the same row % 16, hence the same swizzled piece,
-  // in all of its loads.  The row part of the offset stays in the lane offset, which
-  // the buffer's range check covers (rows past M read zeros); the chunk's position in
-  // the row is the scalar offset.
+  // 4w + 4*WAVES*j + (0..3): a lane keeps the same row % 16, hence the same swizzled
+  // piece, in all of its loads.  The row part of the offset stays in the lane offset,
+  // which the buffer's range check covers (rows past M read zeros); the chunk's
+  // position in the row is the scalar offset.
   static __device__ __forceinline__ void stage(u32x4_t* xb, const QBuffers& bu, const Lanes& ln, int K, int kb,
                                                int wave) {
 #pragma unroll
     for (int j = 0; j < DMA; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(bu.x, (LdsPtr)(xb + (4 * wave + 16 * j) * 16), 16,
-                                               ln.x + static_cast<uint32_t>(j) * 32 * K,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(bu.x, (LdsPtr)(xb + (4 * wave + 4 * WAVES * j) * 16), 16,
+                                               ln.x + static_cast<uint32_t>(j) * (8 * WAVES) * K,
                                                static_cast<uint32_t>(kb) * (kTileK * 2), 0, 0);
   }
 
@@ -264,13 +264,17 @@ __device__ __forceinline__ void chunk_barrier(const u32x4_t* next, uint32_t& tou
 // barrier after chunk c waits for the copy of chunk c + 1, issued XB - 1 chunks
 // earlier; the only weight load issued before that copy and not yet needed is the one
 // for chunk c + 1 itself, so every weight load has XB - 1 chunks to arrive.
-template <int BITS, int GROUP, int MB, int NB, int XB>
-// Two workgroups per CU (two wavefronts per SIMD) fit the LDS of a two-chunk ring; a
-// deeper ring takes one workgroup per CU and may use the SIMD's whole register file.
-__global__ __launch_bounds__(kMmaWaves * kWave) __attribute__((amdgpu_waves_per_eu(XB <= 2 ? 2 : 1)))
-void k_qmma(QArgs a) {
+// WAVES: wavefronts per workgroup, one 32-column block each (NB = 1), all sharing the
+// workgroup's x ring.
+template <int BITS, int GROUP, int MB, int NB, int XB, int WAVES>
+// Four wavefronts: two workgroups per CU (two wavefronts per SIMD) fit the LDS of a
+// two-chunk ring; a deeper ring takes one workgroup per CU and may use the SIMD's
+// whole register file.  Eight wavefronts: one workgroup per CU, two per SIMD.
+__global__ __launch_bounds__(WAVES * kWave)
+__attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(QArgs a) {
   static_assert(XB % 2 == 0 && XB >= 2 && XB <= 6, "chunk parity (pairs of 128-k groups) follows the ring slot");
-  using Body = MmaBody<BITS, GROUP, MB, NB>;
+  static_assert(WAVES == 4 || WAVES == 8, "wavefronts per workgroup");
+  using Body = MmaBody<BITS, GROUP, MB, NB, WAVES>;
   constexpr int GPC = Body::GPC;
   constexpr int XCH = Body::XCH;
   constexpr int PF = XB;
@@ -299,7 +303,7 @@ void k_qmma(QArgs a) {
   int col[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int cb = (ng * kMmaWaves + wave) * NB + nb;
+    const int cb = (ng * WAVES + wave) * NB + nb;
     const int t = 2 * cb + (r32 >> 4);
     ok[nb] = t < a.n_tiles;
     const int tc = ok[nb] ? t : a.n_tiles - 1;
@@ -310,7 +314,7 @@ void k_qmma(QArgs a) {
       ln.w[nb][h] = static_cast<uint32_t>(tc) * a.KB * (256 * BITS) + ((lane & 15) + 16 * (2 * h + hi)) * (4 * BITS);
   }
   {
-    const int row = 4 * wave + (lane >> 4), pc = (lane & 15) ^ row;  // row < 16: its own row % 16
+    const int row = 4 * wave + (lane >> 4), pc = (lane & 15) ^ (row & 15);
     ln.x = (static_cast<uint32_t>(row) * a.K + pc * 8) * 2;
     ln.a = r32 * 16;
     ln.xs = (static_cast<uint32_t>(r32) * ngroups + hi) * 4;
@@ -396,7 +400,7 @@ void k_qmma(QArgs a) {
         const int m = 32 * i + 8 * (r / 4) + 4 * hi + (r % 4);
         if (ok[nb] && m < a.M) store_out(a, wi, m, col[nb], tot[i][nb][r]);
       }
-  if (wi.nsplit > 1) finish_splitk<kMmaWaves * kWave>(a, ng, kMmaWaves * NB * 32);
+  if (wi.nsplit > 1) finish_splitk<WAVES * kWave>(a, ng, WAVES * NB * 32);
 }
 
 }  // namespace qmma
@@ -404,7 +408,7 @@ void k_qmma(QArgs a) {
 typedef void (*QmmaKernel)(QArgs);
 
 struct MmaVariant {
-  int mb, nb, pf, bits, group;  // pf: depth of the x and weight rings (k_qmma's XB)
+  int mb, nb, pf, waves, bits, group;  // pf: depth of the x and weight rings (k_qmma's XB)
   QmmaKernel fn;
 };
 

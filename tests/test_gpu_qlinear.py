@@ -115,6 +115,24 @@ def test_qlinear_balanced_tail_split(M, bits, group):
         assert_close(bf16_to_f64(y), y_ref, f"tail split M={M} bits={bits} g={group} plan={plan}")
 
 
+@pytest.mark.parametrize("M,N,bits,group", [(128, 49152, 3, 128), (65, 49168, 3, 128), (100, 49168, 2, 64),
+                                            (128, 49152, 2, 128)])
+def test_qlinear_eight_wavefront_groups(M, N, bits, group):
+    """256-column groups of eight wavefronts sharing one x ring (the plan for wide
+    launches at M > 64), including a last group with a single 16-column tile (N % 256
+    = 16): every output against the oracle."""
+    K = 384
+    plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
+    assert plan["mfma_rows"] == 32 and plan["waves"] == 8 and plan["col_groups"] == -(-N // 256), plan
+    w = _w(N, K, 320, M, N, bits, group)
+    p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+    q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+    x = synth.activations(M, K, 321, M, N, bits)
+    y = run_qlinear(p, x.to(DEV))
+    y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, group)
+    assert_close(bf16_to_f64(y), y_ref, f"eight wavefronts M={M} N={N} bits={bits} g={group}")
+
+
 @pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32])
 def test_qlinear_exact_integer_case(path):
     # s=1, z=0, codes in {0,1}, x in {-1,0,1}: every partial sum is a small integer,

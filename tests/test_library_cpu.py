@@ -131,17 +131,22 @@ def test_plan_choices_are_consistent():
 def test_mfma_tile_shape_choice():
     """The automatic plan runs 32x32x16 tiles (128 rows) only above M = 64, on launches
     that fill the 256 CUs with whole 128-column groups (two-chunk ring) or split a K of
-    at least 192 blocks (four-chunk ring); everything else stays on 16x16x32 tiles."""
+    at least 192 blocks (four-chunk ring); everything else stays on 16x16x32 tiles.
+    Where 256-column groups still cover three quarters of the CUs and K is not split,
+    eight wavefronts share a four-chunk ring (if that variant is built for the bit
+    width and group)."""
     def shape(M, N, K, bits=3, group=128, path=ss.SUBSPEC_PATH_AUTO):
         p = ss.subspec_qlinear_plan(M, N, K, bits, group, path)
-        return p["mfma_rows"], p["rows"], p["ring_chunks"]
-    assert shape(128, 55296, 5120) == (32, 128, 2)   # 32B gate|up
-    assert shape(96, 37888, 3584, 4) == (32, 128, 2)  # 7B gate|up
-    assert shape(128, 5120, 27648) == (32, 128, 4)   # 32B down
+        return p["mfma_rows"], p["rows"], p["ring_chunks"], p["waves"]
+    assert shape(128, 55296, 5120) == (32, 128, 4, 8)      # 32B gate|up
+    assert shape(128, 55296, 5120, 2, 64) == (32, 128, 4, 8)
+    assert shape(128, 55296, 5120, 4, 128) == (32, 128, 2, 4)  # no eight-wavefront 4-bit build
+    assert shape(96, 37888, 3584, 4) == (32, 128, 2, 4)     # 7B gate|up: 148 groups of 256
+    assert shape(128, 5120, 27648) == (32, 128, 4, 4)      # 32B down
     assert shape(128, 7168, 5120)[0] == 16           # 32B q|k|v
     assert shape(128, 3584, 18944, 4)[0] == 16       # 7B down
     assert shape(64, 55296, 5120)[0] == 16
-    assert shape(17, 512, 256, path=ss.SUBSPEC_PATH_MFMA32) == (32, 128, 4)
+    assert shape(17, 512, 256, path=ss.SUBSPEC_PATH_MFMA32) == (32, 128, 4, 4)
     assert shape(128, 55296, 5120, path=ss.SUBSPEC_PATH_MFMA16)[0] == 16
     for path in (ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32):
         assert ss.subspec_qlinear_plan(40, 512, 256, 4, 64, path)["path"] == ss.SUBSPEC_PATH_MFMA
