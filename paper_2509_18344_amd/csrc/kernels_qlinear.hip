@@ -338,14 +338,17 @@ void k_qgemm_mfma(QArgs a) {
   // (weights of chunk c+PF, then activations of chunk c+1+PF), so every load is
   // issued PF chunks before it is waited for.  Loads complete in issue order: an
   // activation ring shallower than the weight ring would cap the weights' lead too.
+  // Loads of chunks past the split repeat its last chunk (L2 hits, never consumed),
+  // so a split shorter than the ring costs no extra memory traffic.
   typename Body::W w[PF];
   typename Body::X x[PF];
+  const int kb_last = kb0 + (nchunks - 1) * CH;
   static_for<PF>([&](auto u) __attribute__((always_inline)) {
-    Body::load_w(w[u.value], bu, a, wofs, col, kb0 + u.value * CH);
-    Body::stage_load(x[u.value], bu, a.K, kb0 + u.value * CH);
+    Body::load_w(w[u.value], bu, a, wofs, col, min(kb0 + u.value * CH, kb_last));
+    Body::stage_load(x[u.value], bu, a.K, min(kb0 + u.value * CH, kb_last));
   });
   Body::stage_store(lds, 0, x[0]);
-  Body::stage_load(x[0], bu, a.K, kb0 + PF * CH);
+  Body::stage_load(x[0], bu, a.K, min(kb0 + PF * CH, kb_last));
   // The first chunk's zero-point step reads the sums of "chunk -1": zeros, with
   // zero offsets.
   for (int i = threadIdx.x; i < GPC * Body::ROWS; i += WAVES * kWave) (&lds.xs[1][0][0])[i] = 0.f;
@@ -383,9 +386,9 @@ void k_qgemm_mfma(QArgs a) {
         Body::template correct<FULL>(lds, (U + 1) & 1, kb - CH, kb_end, lane, cprev, tot);
         Body::template compute<FULL, DW>(w[U], lds, U & 1, kb, kb_end, lane, tot, cprev);
       }
-      if constexpr (FULL) Body::load_w(w[U], bu, a, wofs, col, kb + PF * CH);
+      if constexpr (FULL) Body::load_w(w[U], bu, a, wofs, col, min(kb + PF * CH, kb_last));
       Body::stage_store(lds, (U + 1) & 1, x[V]);
-      if constexpr (FULL) Body::stage_load(x[V], bu, a.K, kb + (PF + 1) * CH);
+      if constexpr (FULL) Body::stage_load(x[V], bu, a.K, min(kb + (PF + 1) * CH, kb_last));
       __syncthreads();
     };
     // Steady state: straight-line body (every load unconditional) so that each wait
@@ -593,10 +596,13 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
       szs[p] = __builtin_amdgcn_raw_buffer_load_b128(bu.s, off, 0, 0);
       szz[p] = __builtin_amdgcn_raw_buffer_load_b128(bu.z, off, 0, 0);
     }
-    // The weight stream starts right after these (small) loads with one chunk: loads
-    // complete in issue order, and a smaller first burst lets the activations (which
-    // every wavefront needs before it can start) return sooner.
-    Body::load(w[0], bu.w, wofs, 0);
+    // The whole weight ring is issued right after these (small) loads: they complete
+    // in issue order, so the activations still return first, and a short split then
+    // waits for one memory latency instead of one per ring refill.  Chunks past the
+    // split repeat its last one (L2 hits, never consumed).
+    static_for<PF>([&](auto u) __attribute__((always_inline)) {
+      Body::load(w[u.value], bu.w, wofs, min(u.value, nchunks - 1) * CH);
+    });
 #pragma unroll
     for (int p = 0; p < kGemvSpans; ++p) {
       const int i = p * THREADS + threadIdx.x;
@@ -633,10 +639,6 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
   }
   __syncthreads();
 
-  static_for<PF - 1>([&](auto u) __attribute__((always_inline)) {
-    Body::load(w[u.value + 1], bu.w, wofs, (u.value + 1) * CH);
-  });
-
   float tot[ROWS][NT];
 #pragma unroll
   for (int m = 0; m < ROWS; ++m)
@@ -649,7 +651,7 @@ __global__ __launch_bounds__(WAVES * kWave) void k_qgemv(QArgs a) {
     static_for<PF>([&](auto u) __attribute__((always_inline)) {
       constexpr int U = decltype(u)::value;
       Body::compute(w[U], xl, xsum, sc, xs, COLS, (c + U) * CH, nblk, quarter, lcol, tot);
-      Body::load(w[U], bu.w, wofs, (c + U + PF) * CH);
+      Body::load(w[U], bu.w, wofs, min(c + U + PF, nchunks - 1) * CH);
     });
   }
   static_for<PF>([&](auto u) __attribute__((always_inline)) {
