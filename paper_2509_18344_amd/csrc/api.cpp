@@ -93,6 +93,9 @@ struct Tuning {
   int mma_nb = 0;                 // 32x32 kernel: 32-column blocks per wavefront; 0 = choose
   int mma_shape = 0;              // automatic MFMA plans: 16 or 32 forces the tile shape
   int mma_waves = 0;              // 32x32 kernel: wavefronts per workgroup (4 or 8); 0 = choose
+  // Smallest M at which wide launches take the 32x32 kernel's 64-row eight-wavefront
+  // tiles instead of 16x16x32 ones (0 = never).
+  int mma8_min_m = 33;
 };
 
 // Optional overrides for measurement sweeps: SUBSPEC_TUNE="gemv_max_m=4,target=512,...".
@@ -129,6 +132,7 @@ const Tuning& tuning() {
         else if (k == "mma_nb") r.mma_nb = v;
         else if (k == "mma_shape") r.mma_shape = v;
         else if (k == "mma_waves") r.mma_waves = v;
+        else if (k == "mma8_min_m") r.mma8_min_m = v;
       }
       pos = end + 1;
     }
@@ -182,8 +186,16 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   // 16x16x32 kernel is faster (7B o at M = 128: 25.8 against 32.0 us).
   const bool wide = (N + 127) / 128 >= device_cus();
   const bool long_k = KB >= 192;
+  // 256-column groups (eight wavefronts of the 32x32 kernel) still cover three
+  // quarters of the CUs.
+  const bool wide8 = (N + 255) / 256 * 4 >= 3 * device_cus();
   if (path == SUBSPEC_PATH_MFMA) {
-    const bool use32 = tu.mma_shape ? tu.mma_shape == 32 : M > tu.mma16_max_m && (wide || long_k);
+    // Below mma16_max_m, wide unsplit launches still take 64-row 32x32 tiles from
+    // mma8_min_m on: 32B gate|up 48.7 against 53.4 us at M = 33, 51.6 against 55.1 at
+    // 48, 53.9 against 59.0 at 64; the short and the long-K launches stay on 16x16x32
+    // (q|k|v at M = 64 27.2 against 19.0 us, down 48.1 against 41.0).
+    const bool tiles64 = tu.mma8_min_m > 0 && M >= tu.mma8_min_m && wide8 && !long_k;
+    const bool use32 = tu.mma_shape ? tu.mma_shape == 32 : (M > tu.mma16_max_m && (wide || long_k)) || tiles64;
     path = use32 ? SUBSPEC_PATH_MFMA32 : SUBSPEC_PATH_MFMA16;
   }
   subspec::KernelChoice c{}, c8{};
@@ -206,7 +218,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     // deep (one workgroup per CU, more loads in flight each) when K is split.
     c.path = 2;
     c.shape = 32;
-    c.rows = 128;
+    c.rows = M <= 64 ? 64 : 128;
     c.nt = 2 * (tu.mma_nb ? tu.mma_nb : 1);
     c.chunk = 1;
     c.prefetch = tu.mfma_pf ? tu.mfma_pf : wide ? 2 : 4;
@@ -215,8 +227,8 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     // weights in flight instead of one.  Taken where 256-column groups still cover
     // three quarters of the CUs and K is not split (32B gate|up, N = 55296, M = 128:
     // 90.9 against 98.0 us at 3 bits, 97.1 against 103.1 at 2 bits; slower on the 7B
-    // gate|up's 148 groups and on the split 32B down projection).
-    const bool wide8 = (N + 255) / 256 * 4 >= 3 * device_cus();
+    // gate|up's 148 groups and on the split 32B down projection).  Up to M = 64 the
+    // tiles are 64 rows (two row blocks), built for eight wavefronts only.
     c8 = c;
     c8.waves = 8;
     c8.prefetch = tu.mfma_pf ? tu.mfma_pf : 4;
@@ -240,6 +252,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
                          : subspec::qlinear_variant_exists(k, bits, group);
   };
   if (use8 && (tu.mma_waves == 8 || variant_exists(c8))) c = c8;
+  if (c.shape == 32 && c.rows == 64 && !variant_exists(c)) c.rows = 128;  // no 64-row build
   if (!variant_exists(c))
     return fail(SUBSPEC_EUNSUPPORTED, "no kernel for path=%d rows=%d nt=%d chunk=%d waves=%d bits=%d group=%d",
                 c.path, c.rows, c.nt, c.chunk, c.waves, bits, group);

@@ -11,6 +11,7 @@ namespace subspec {
 static const MmaVariant kVariants[] = {
     SUBSPEC_QMMA(128, 4, 1, 2, 4), SUBSPEC_QMMA(128, 4, 1, 4, 4), SUBSPEC_QMMA(128, 4, 1, 4, 8),
     SUBSPEC_QMMA(64, 4, 1, 2, 4),  SUBSPEC_QMMA(64, 4, 1, 4, 4),  SUBSPEC_QMMA(64, 4, 1, 4, 8),
+    SUBSPEC_QMMA(128, 2, 1, 4, 8), SUBSPEC_QMMA(64, 2, 1, 4, 8),
 };
 
 const MmaVariant* qmma_variants_b2(int* n) {

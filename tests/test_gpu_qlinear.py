@@ -116,14 +116,17 @@ def test_qlinear_balanced_tail_split(M, bits, group):
 
 
 @pytest.mark.parametrize("M,N,bits,group", [(128, 49152, 3, 128), (65, 49168, 3, 128), (100, 49168, 2, 64),
-                                            (128, 49152, 2, 128)])
+                                            (128, 49152, 2, 128), (64, 49152, 3, 128), (33, 49168, 4, 64),
+                                            (48, 49168, 2, 128), (40, 49152, 4, 128)])
 def test_qlinear_eight_wavefront_groups(M, N, bits, group):
     """256-column groups of eight wavefronts sharing one x ring (the plan for wide
-    launches at M > 64), including a last group with a single 16-column tile (N % 256
-    = 16): every output against the oracle."""
+    launches from M = 33: 64-row tiles up to M = 64, 128-row ones above), including a
+    last group with a single 16-column tile (N % 256 = 16): every output against the
+    oracle."""
     K = 384
     plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
     assert plan["mfma_rows"] == 32 and plan["waves"] == 8 and plan["col_groups"] == -(-N // 256), plan
+    assert plan["rows"] == (64 if M <= 64 else 128), plan
     w = _w(N, K, 320, M, N, bits, group)
     p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
     q, s16, z16 = oracle.quantize_minmax(w, bits, group)

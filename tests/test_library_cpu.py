@@ -134,7 +134,7 @@ def test_mfma_tile_shape_choice():
     at least 192 blocks (four-chunk ring); everything else stays on 16x16x32 tiles.
     Where 256-column groups still cover three quarters of the CUs and K is not split,
     eight wavefronts share a four-chunk ring (if that variant is built for the bit
-    width and group)."""
+    width and group), and from M = 33 such launches take 64-row 32x32x16 tiles too."""
     def shape(M, N, K, bits=3, group=128, path=ss.SUBSPEC_PATH_AUTO):
         p = ss.subspec_qlinear_plan(M, N, K, bits, group, path)
         return p["mfma_rows"], p["rows"], p["ring_chunks"], p["waves"]
@@ -145,7 +145,13 @@ def test_mfma_tile_shape_choice():
     assert shape(128, 5120, 27648) == (32, 128, 4, 4)      # 32B down
     assert shape(128, 7168, 5120)[0] == 16           # 32B q|k|v
     assert shape(128, 3584, 18944, 4)[0] == 16       # 7B down
-    assert shape(64, 55296, 5120)[0] == 16
+    assert shape(64, 55296, 5120) == (32, 64, 4, 8)        # 32B gate|up, 64-row tiles
+    assert shape(33, 55296, 5120, 2, 64) == (32, 64, 4, 8)
+    assert shape(48, 55296, 5120, 4, 128) == (32, 64, 4, 8)
+    assert shape(32, 55296, 5120)[0] == 16
+    assert shape(64, 37888, 3584, 4)[0] == 16              # 7B gate|up: not wide enough
+    assert shape(64, 5120, 27648)[0] == 16                 # long K
+    assert shape(64, 7168, 5120)[0] == 16                  # q|k|v
     assert shape(17, 512, 256, path=ss.SUBSPEC_PATH_MFMA32) == (32, 128, 4, 4)
     assert shape(128, 55296, 5120, path=ss.SUBSPEC_PATH_MFMA16)[0] == 16
     for path in (ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32):
