@@ -85,8 +85,9 @@ enum subspec_path {
   SUBSPEC_PATH_MFMA = 2, /* bf16 matrix cores on unpacked code tiles; any M; the
                             plan picks the instruction shape (below)             */
   SUBSPEC_PATH_MFMA16 = 3, /* MFMA path on 16x16x32 instructions (row tiles of 16) */
-  SUBSPEC_PATH_MFMA32 = 4  /* MFMA path on 32x32x16 instructions, always 128 rows
-                              (four row blocks of 32; rows past M are padding)   */
+  SUBSPEC_PATH_MFMA32 = 4  /* MFMA path on 32x32x16 instructions, 128 rows (four
+                              row blocks of 32), or 64 where M <= 64 and the
+                              eight-wavefront kernel runs; rows past M are padding */
 };
 
 /* Launch configuration chosen for one qlinear call (host-side description). */
@@ -94,9 +95,11 @@ typedef struct subspec_plan {
   int path;            /* SUBSPEC_PATH_GEMV or SUBSPEC_PATH_MFMA                  */
   int mfma_rows;       /* MFMA path: 16 (16x16x32 bf16 instructions) or 32
                           (32x32x16 bf16); 0 on the GEMV path.  The automatic
-                          choice takes 32 only for M > 64 and launches that either
-                          fill every CU with whole 128-column groups or split a K
-                          of at least 24576 (measured on the Qwen2.5 shapes)     */
+                          choice takes 32 for M > 64 on launches that either fill
+                          every CU with whole 128-column groups or split a K of at
+                          least 24576, and for 32 < M <= 64 on launches whose
+                          256-column groups cover three quarters of the CUs with K
+                          unsplit (measured on the Qwen2.5 shapes)               */
   int rows;            /* rows computed per workgroup (M rounded up)              */
   int tiles_per_wave;  /* 16-column tiles each wavefront owns                     */
   int waves;           /* wavefronts per workgroup                                */
