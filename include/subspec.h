@@ -97,7 +97,7 @@ typedef struct subspec_plan {
                           (32x32x16 bf16); 0 on the GEMV path.  The automatic
                           choice takes 32 for M > 64 on launches that either fill
                           every CU with whole 128-column groups or split a K of at
-                          least 24576, and for 32 < M <= 64 on launches whose
+                          least 16384, and for 32 < M <= 64 on launches whose
                           256-column groups cover three quarters of the CUs with K
                           unsplit (measured on the Qwen2.5 shapes)               */
   int rows;            /* rows computed per workgroup (M rounded up)              */
@@ -106,7 +106,7 @@ typedef struct subspec_plan {
   int chunk_blocks;    /* 128-k blocks staged in LDS per step                     */
   int ring_chunks;     /* MFMA path: chunks of weights in each wavefront's register
                           ring (0 = the kernel's default; GEMV: ring stages)     */
-  int col_groups;      /* column groups (waves * tiles_per_wave * 16 columns each) */
+  int col_groups;      /* column groups (waves / teams * tiles_per_wave * 16 columns each) */
   int full_groups;     /* column groups [0, full_groups) run whole, one workgroup
                           each; the others are split along K                    */
   int splits;          /* workgroups per split column group; 1 = no partial sums  */
@@ -117,6 +117,10 @@ typedef struct subspec_plan {
                              counters, the 32x32 kernel's per-group sums of x, and
                              the fp32 partial sums of split column groups (0 when
                              none of these is needed) */
+  int teams;           /* 32-row MFMA tiles: wavefront teams per workgroup that split
+                          its k-blocks between them (1, or 2: two teams of four on
+                          the same columns, summed in LDS); a workgroup covers
+                          waves / teams * tiles_per_wave * 16 columns             */
 } subspec_plan;
 
 /* Bytes of the packed code buffer for an N x K projection.  0 on bad arguments. */

@@ -33,7 +33,8 @@ class _Plan(ctypes.Structure):
                 ("chunk_blocks", ctypes.c_int), ("ring_chunks", ctypes.c_int), ("col_groups", ctypes.c_int),
                 ("full_groups", ctypes.c_int),
                 ("splits", ctypes.c_int), ("blocks_per_split", ctypes.c_int),
-                ("grid", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t)]
+                ("grid", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t),
+                ("teams", ctypes.c_int)]
 
 
 class SubspecProj(ctypes.Structure):

@@ -96,6 +96,7 @@ struct Tuning {
   // Smallest M at which wide launches take the 32x32 kernel's 64-row eight-wavefront
   // tiles instead of 16x16x32 ones (0 = never).
   int mma8_min_m = 33;
+  int mma_teams = 0;              // 32x32 kernel, long-K launches: 1 = one team, 2 = two; 0 = choose
 };
 
 // Optional overrides for measurement sweeps: SUBSPEC_TUNE="gemv_max_m=4,target=512,...".
@@ -133,6 +134,7 @@ const Tuning& tuning() {
         else if (k == "mma_shape") r.mma_shape = v;
         else if (k == "mma_waves") r.mma_waves = v;
         else if (k == "mma8_min_m") r.mma8_min_m = v;
+        else if (k == "mma_teams") r.mma_teams = v;
       }
       pos = end + 1;
     }
@@ -185,7 +187,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   // against 68.2 us); on the short split launches (q|k|v, o; 7B down, K = 18944) the
   // 16x16x32 kernel is faster (7B o at M = 128: 25.8 against 32.0 us).
   const bool wide = (N + 127) / 128 >= device_cus();
-  const bool long_k = KB >= 192;
+  const bool long_k = KB >= 128;
   // 256-column groups (eight wavefronts of the 32x32 kernel) still cover three
   // quarters of the CUs.
   const bool wide8 = (N + 255) / 256 * 4 >= 3 * device_cus();
@@ -212,10 +214,12 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c.chunk = tu.gemv_ch ? tu.gemv_ch : c.rows <= 2 ? 2 : 4;
     c.prefetch = tu.gemv_pf;
   } else if (path == SUBSPEC_PATH_MFMA32) {
-    // 32x32x16 matrix cores (k_qmma): four row blocks of 32, four wavefronts of one
-    // 32-column block each, one 128-k chunk per LDS stage.  The ring is two chunks
-    // deep (two workgroups per CU) when whole column groups fill the device, four
-    // deep (one workgroup per CU, more loads in flight each) when K is split.
+    // 32x32x16 matrix cores (k_qmma): four row blocks of 32 (two up to M = 64), four
+    // wavefronts of one 32-column block each, one 128-k chunk per LDS stage.  The ring
+    // is two chunks deep (two workgroups per CU) when whole column groups fill the
+    // device, four deep (one workgroup per CU, more loads in flight each) otherwise;
+    // the eight-wavefront and two-team forms below replace it where they measured
+    // faster.
     c.path = 2;
     c.shape = 32;
     c.rows = M <= 64 ? 64 : 128;
@@ -233,6 +237,19 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c8.waves = 8;
     c8.prefetch = tu.mfma_pf ? tu.mfma_pf : 4;
     use8 = tu.mma_waves == 8 || (!tu.mma_waves && wide8 && !long_k);
+    // Long-K launches (split along K, not wide enough for whole groups) take two teams
+    // of four wavefronts per workgroup, each on half of the workgroup's k-blocks: two
+    // wavefronts per SIMD at the same number of splits (32B down, K = 27648: 61.5
+    // against 63.8 us at M = 128, 54.7 against 58.7 at 96; 7B down, K = 18944: 40.5
+    // against 45.7 on 16x16x32 tiles at M = 128).
+    const bool teams = tu.mma_teams ? tu.mma_teams == 2 : long_k;
+    if (!use8 && teams && c.rows == 128) {
+      c8 = c;
+      c8.waves = 8;
+      c8.teams = 2;
+      c8.prefetch = 2;
+      use8 = true;
+    }
   } else if (path == SUBSPEC_PATH_MFMA16) {
     c.path = 2;
     c.shape = 16;
@@ -248,7 +265,8 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     return fail(SUBSPEC_EINVAL, "path=%d: unknown", path);
   }
   auto variant_exists = [&](const subspec::KernelChoice& k) {
-    return k.shape == 32 ? subspec::qmma_variant_exists(k.waves, k.rows / 32, k.nt / 2, k.prefetch, bits, group)
+    return k.shape == 32 ? subspec::qmma_variant_exists(k.waves, k.teams, k.rows / 32, k.nt / 2, k.prefetch, bits,
+                                                        group)
                          : subspec::qlinear_variant_exists(k, bits, group);
   };
   if (use8 && (tu.mma_waves == 8 || variant_exists(c8))) c = c8;
@@ -262,18 +280,18 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     if (tu.target_blocks > 0) return tu.target_blocks;
     size_t lds = 0;
     if (k.path == 1) {
-      const int cols = k.waves * k.nt * subspec::kTileN;
+      const int cols = k.waves / k.teams * k.nt * subspec::kTileN;
       lds = subspec::gemv_lds_bytes(k.rows, std::min(K, subspec::gemv_max_kspan(k.rows, k.waves, group, cols)),
                                     group, cols);
     }
-    int per_cu = k.shape == 32 ? subspec::qmma_resident_blocks(k.waves, k.rows / 32, k.nt / 2, k.prefetch, bits,
-                                                               group)
+    int per_cu = k.shape == 32 ? subspec::qmma_resident_blocks(k.waves, k.teams, k.rows / 32, k.nt / 2,
+                                                               k.prefetch, bits, group)
                                : subspec::qlinear_resident_blocks(k, bits, group, lds);
     if (per_cu <= 0) per_cu = 2;
     return per_cu * device_cus();
   };
   auto groups_of = [&](const subspec::KernelChoice& k) {
-    const int cols = k.waves * k.nt * subspec::kTileN;
+    const int cols = k.waves / k.teams * k.nt * subspec::kTileN;
     return (N + cols - 1) / cols;
   };
   int resident = resident_of(c);
@@ -299,7 +317,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
       }
     }
   }
-  const int cols_per_group = c.waves * c.nt * subspec::kTileN;
+  const int cols_per_group = c.waves / c.teams * c.nt * subspec::kTileN;
   const int col_groups = groups_of(c);
   const int chunks = (KB + c.chunk - 1) / c.chunk;
 
@@ -384,6 +402,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   }
   p->path = c.path == 1 ? SUBSPEC_PATH_GEMV : SUBSPEC_PATH_MFMA;
   p->mfma_rows = c.path == 2 ? c.shape : 0;
+  p->teams = c.teams;
   p->rows = c.rows;
   p->tiles_per_wave = c.nt;
   p->waves = c.waves;
@@ -619,7 +638,8 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
   if (kc.shape == 32) {
     e = subspec::launch_xsum(a.x, M, K, group, const_cast<float*>(a.xsum), st);
     if (e == hipSuccess)
-      e = subspec::launch_qmma(kc.waves, kc.rows / 32, kc.nt / 2, kc.prefetch, bits, group, a, p.grid, st);
+      e = subspec::launch_qmma(kc.waves, kc.teams, kc.rows / 32, kc.nt / 2, kc.prefetch, bits, group, a, p.grid,
+                               st);
   } else {
     e = subspec::launch_qlinear(kc, bits, group, a, p.grid, st);
   }

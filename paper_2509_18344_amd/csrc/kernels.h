@@ -42,6 +42,7 @@ struct KernelChoice {
   int waves;   // wavefronts per workgroup (4 or 8)
   int prefetch = 0;  // ring depth in chunks; 0 = the variant table's choice
   int shape = 0;     // MFMA path: 16 = k_qgemm_mfma (16x16x32), 32 = k_qmma (32x32x16)
+  int teams = 1;     // k_qmma: wavefront teams splitting the workgroup's K range
 };
 
 hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a,
@@ -55,12 +56,13 @@ int qlinear_resident_blocks(const KernelChoice& kc, int bits, int group, size_t 
 int gemv_max_kspan(int rows, int waves, int group, int cols);
 size_t gemv_lds_bytes(int rows, int kspan, int group, int cols);
 
-// The 32x32x16 kernel (k_qmma): `waves` wavefronts per workgroup (4 or 8), mb 32-row
-// blocks, nb 32-column blocks per wavefront, a ring of pf chunks.
-bool qmma_variant_exists(int waves, int mb, int nb, int pf, int bits, int group);
-int qmma_resident_blocks(int waves, int mb, int nb, int pf, int bits, int group);
-hipError_t launch_qmma(int waves, int mb, int nb, int pf, int bits, int group, const QArgs& a, int grid,
-                       hipStream_t st);
+// The 32x32x16 kernel (k_qmma): `waves` wavefronts per workgroup (4 or 8) in `teams`
+// teams that split its K range (1 or 2), mb 32-row blocks, nb 32-column blocks per
+// wavefront, a ring of pf chunks.
+bool qmma_variant_exists(int waves, int teams, int mb, int nb, int pf, int bits, int group);
+int qmma_resident_blocks(int waves, int teams, int mb, int nb, int pf, int bits, int group);
+hipError_t launch_qmma(int waves, int teams, int mb, int nb, int pf, int bits, int group, const QArgs& a,
+                       int grid, hipStream_t st);
 // The sums of x over every group of k that k_qmma needs: out[m][g] = sum over the
 // group's k of x[m][k] (fp32), x bf16 [M][K].
 hipError_t launch_xsum(const uint16_t* x, int M, int K, int group, float* out, hipStream_t st);

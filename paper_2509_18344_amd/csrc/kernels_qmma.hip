@@ -3,22 +3,22 @@
 
 namespace subspec {
 
-static const MmaVariant* find_mma(int waves, int mb, int nb, int pf, int bits, int group) {
+static const MmaVariant* find_mma(int waves, int teams, int mb, int nb, int pf, int bits, int group) {
   int n = 0;
   const MmaVariant* v = bits == 2 ? qmma_variants_b2(&n) : bits == 3 ? qmma_variants_b3(&n) : qmma_variants_b4(&n);
   for (int i = 0; i < n; ++i)
-    if (v[i].waves == waves && v[i].mb == mb && v[i].nb == nb && (pf == 0 || v[i].pf == pf) && v[i].bits == bits &&
+    if (v[i].waves == waves && v[i].teams == teams && v[i].mb == mb && v[i].nb == nb && (pf == 0 || v[i].pf == pf) && v[i].bits == bits &&
         v[i].group == group)
       return &v[i];
   return nullptr;
 }
 
-bool qmma_variant_exists(int waves, int mb, int nb, int pf, int bits, int group) {
-  return find_mma(waves, mb, nb, pf, bits, group) != nullptr;
+bool qmma_variant_exists(int waves, int teams, int mb, int nb, int pf, int bits, int group) {
+  return find_mma(waves, teams, mb, nb, pf, bits, group) != nullptr;
 }
 
-int qmma_resident_blocks(int waves, int mb, int nb, int pf, int bits, int group) {
-  const MmaVariant* v = find_mma(waves, mb, nb, pf, bits, group);
+int qmma_resident_blocks(int waves, int teams, int mb, int nb, int pf, int bits, int group) {
+  const MmaVariant* v = find_mma(waves, teams, mb, nb, pf, bits, group);
   if (!v) return 0;
   int blocks = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, reinterpret_cast<const void*>(v->fn),
@@ -29,9 +29,9 @@ int qmma_resident_blocks(int waves, int mb, int nb, int pf, int bits, int group)
   return blocks;
 }
 
-hipError_t launch_qmma(int waves, int mb, int nb, int pf, int bits, int group, const QArgs& a, int grid,
-                       hipStream_t st) {
-  const MmaVariant* v = find_mma(waves, mb, nb, pf, bits, group);
+hipError_t launch_qmma(int waves, int teams, int mb, int nb, int pf, int bits, int group, const QArgs& a,
+                       int grid, hipStream_t st) {
+  const MmaVariant* v = find_mma(waves, teams, mb, nb, pf, bits, group);
   if (!v) return hipErrorInvalidDeviceFunction;
   hipLaunchKernelGGL(v->fn, dim3(grid), dim3(waves * kWave), 0, st, a);
   return hipGetLastError();

@@ -3,7 +3,8 @@
 
 namespace subspec {
 
-#define SUBSPEC_QMMA(G, MB, NB, PF, W) {MB, NB, PF, W, 2, G, qmma::k_qmma<2, G, MB, NB, PF, W>}
+#define SUBSPEC_QMMA(G, MB, NB, PF, W) {MB, NB, PF, W, 1, 2, G, qmma::k_qmma<2, G, MB, NB, PF, W, 1>}
+#define SUBSPEC_QMMA_TEAMS(G) {4, 1, 2, 8, 2, 2, G, qmma::k_qmma<2, G, 4, 1, 2, 8, 2>}
 
 // Four row blocks (M = 65..128).  Four wavefronts with the ring two chunks deep (two
 // workgroups per CU) or four (one workgroup per CU, for launches split along a long K);
@@ -12,6 +13,7 @@ static const MmaVariant kVariants[] = {
     SUBSPEC_QMMA(128, 4, 1, 2, 4), SUBSPEC_QMMA(128, 4, 1, 4, 4), SUBSPEC_QMMA(128, 4, 1, 4, 8),
     SUBSPEC_QMMA(64, 4, 1, 2, 4),  SUBSPEC_QMMA(64, 4, 1, 4, 4),  SUBSPEC_QMMA(64, 4, 1, 4, 8),
     SUBSPEC_QMMA(128, 2, 1, 4, 8), SUBSPEC_QMMA(64, 2, 1, 4, 8),
+    SUBSPEC_QMMA_TEAMS(128), SUBSPEC_QMMA_TEAMS(64),
 };
 
 const MmaVariant* qmma_variants_b2(int* n) {

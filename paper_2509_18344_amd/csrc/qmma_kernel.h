@@ -264,9 +264,12 @@ __device__ __forceinline__ void chunk_barrier(const u32x4_t* next, uint32_t& tou
 // barrier after chunk c waits for the copy of chunk c + 1, issued XB - 1 chunks
 // earlier; the only weight load issued before that copy and not yet needed is the one
 // for chunk c + 1 itself, so every weight load has XB - 1 chunks to arrive.
-// WAVES: wavefronts per workgroup, one 32-column block each (NB = 1), all sharing the
-// workgroup's x ring.
-template <int BITS, int GROUP, int MB, int NB, int XB, int WAVES>
+// WAVES: wavefronts per workgroup, one 32-column block each (NB = 1).  TEAMS = 1: all
+// of them share the workgroup's x ring.  TEAMS = 2: two teams of four wavefronts on
+// the same four column blocks, each with an x ring of its own, take the first and the
+// second half of the workgroup's k-blocks, and add their sums through LDS in team
+// order at the end (twice the wavefronts per column group without more partial sums).
+template <int BITS, int GROUP, int MB, int NB, int XB, int WAVES, int TEAMS>
 // Four wavefronts: two workgroups per CU (two wavefronts per SIMD) fit the LDS of a
 // two-chunk ring; a deeper ring takes one workgroup per CU and may use the SIMD's
 // whole register file.  Eight wavefronts: one workgroup per CU, two per SIMD.
@@ -274,12 +277,16 @@ __global__ __launch_bounds__(WAVES * kWave)
 __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(QArgs a) {
   static_assert(XB % 2 == 0 && XB >= 2 && XB <= 6, "chunk parity (pairs of 128-k groups) follows the ring slot");
   static_assert(WAVES == 4 || WAVES == 8, "wavefronts per workgroup");
-  using Body = MmaBody<BITS, GROUP, MB, NB, WAVES>;
+  static_assert(TEAMS == 1 || (TEAMS == 2 && WAVES == 8 && XB == 2 && MB == 4 && NB == 1),
+                "two teams of four wavefronts with two-chunk rings");
+  constexpr int TW = WAVES / TEAMS;  // wavefronts per team (its column blocks)
+  using Body = MmaBody<BITS, GROUP, MB, NB, TW>;
   constexpr int GPC = Body::GPC;
   constexpr int XCH = Body::XCH;
   constexpr int PF = XB;
-  __shared__ u32x4_t xb0[XCH], xb1[XCH], xb2[XB > 2 ? XCH : 1], xb3[XB > 3 ? XCH : 1], xb4[XB > 4 ? XCH : 1],
-      xb5[XB > 5 ? XCH : 1];
+  constexpr int NBUF = XB * TEAMS;  // LDS chunk buffers; team t uses [t * XB, t * XB + XB)
+  __shared__ u32x4_t xb0[XCH], xb1[XCH], xb2[NBUF > 2 ? XCH : 1], xb3[NBUF > 3 ? XCH : 1],
+      xb4[NBUF > 4 ? XCH : 1], xb5[NBUF > 5 ? XCH : 1];
   auto& b2 = reinterpret_cast<u32x4_t(&)[XCH]>(xb2);
   auto& b3 = reinterpret_cast<u32x4_t(&)[XCH]>(xb3);
   auto& b4 = reinterpret_cast<u32x4_t(&)[XCH]>(xb4);
@@ -287,13 +294,26 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
 
   const int lane = threadIdx.x % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
+  const int team = wave / TW, tw = wave % TW;
   const int r32 = lane & 31, hi = lane >> 5;
   const WorkItem wi(a);
-  const int ng = wi.ng, kb0 = wi.kb0;
-  const int nchunks = wi.kb_end - wi.kb0;  // one 128-k block per chunk
+  const int ng = wi.ng;
+  // The team's k-blocks: team 0 the first half of the workgroup's (rounded up), team 1
+  // the rest (possibly none).  Both run team 0's number of chunk steps, so that their
+  // barriers pair up; a team past its last chunk skips the arithmetic.
+  const int nwg = wi.kb_end - wi.kb0;
+  const int h0 = TEAMS == 1 ? nwg : (nwg + 1) / 2;
+  const int kb0 = wi.kb0 + (team == 0 ? 0 : h0);
+  const int nchunks = team == 0 ? h0 : nwg - h0;
+  const int nsteps = h0;
   const int last = nchunks - 1;
   const int ngroups = a.K / GROUP;
   const QBuffers bu(a, BITS, GROUP);
+  // Block of the team's chunk c, held inside the workgroup's range: loads past the
+  // team's last chunk repeat it (L2 hits, never used).
+  auto blk = [&](int c) __attribute__((always_inline)) {
+    return min(kb0 + max(min(c, last), 0), wi.kb_end - 1);
+  };
 
   // Column blocks of this wavefront: 32 columns each, tiles 2cb and 2cb + 1.  A
   // block past N (half of the last one when N % 32 == 16) reads a valid tile and is
@@ -303,7 +323,7 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
   int col[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int cb = (ng * WAVES + wave) * NB + nb;
+    const int cb = (ng * TW + tw) * NB + nb;
     const int t = 2 * cb + (r32 >> 4);
     ok[nb] = t < a.n_tiles;
     const int tc = ok[nb] ? t : a.n_tiles - 1;
@@ -314,7 +334,7 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
       ln.w[nb][h] = static_cast<uint32_t>(tc) * a.KB * (256 * BITS) + ((lane & 15) + 16 * (2 * h + hi)) * (4 * BITS);
   }
   {
-    const int row = 4 * wave + (lane >> 4), pc = (lane & 15) ^ (row & 15);
+    const int row = 4 * tw + (lane >> 4), pc = (lane & 15) ^ (row & 15);
     ln.x = (static_cast<uint32_t>(row) * a.K + pc * 8) * 2;
     ln.a = r32 * 16;
     ln.xs = (static_cast<uint32_t>(r32) * ngroups + hi) * 4;
@@ -328,79 +348,128 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
 
   // The first group of the pair whose x sums chunk c's ring slot carries: with groups
   // of 64 its own two groups; with groups of 128 the pair (c - 1, c) for odd c and
-  // (c, c + 1) for even c (used only when c is the split's last chunk, then alone).
+  // (c, c + 1) for even c (used only when c is the team's last chunk, then alone).  A
+  // refill past the last chunk can ask for group -1 of the workgroup's first block,
+  // which it never uses: held at 0, since the scalar offset of a buffer load is not
+  // range checked.
   auto pair_first = [&](int c, int parity) __attribute__((always_inline)) {
-    const int kb = kb0 + c;
-    return GPC == 2 ? 2 * kb : parity ? kb - 1 : kb;
+    const int kb = blk(c);
+    return GPC == 2 ? 2 * kb : parity ? max(kb - 1, 0) : kb;
   };
 
-  // Prologue: chunks 0 .. XB - 2 of x and of the weights in flight.  Chunks past the
-  // split repeat its last one (an L2 hit, never used): unconditional loads keep the
-  // compiler's count of outstanding loads exact.
-  typename Body::W w[PF];
   uint32_t touch = 0;
-  static_for<XB - 1>([&](auto u) __attribute__((always_inline)) {
-    constexpr int U = decltype(u)::value;
-    const int c = min(U, last);
-    Body::stage(xring<XB, U>(xb0, xb1, b2, b3, b4, b5), bu, ln, a.K, kb0 + c, wave);
-    Body::load_w(w[U], bu, ln, a.N, kb0 + c, pair_first(c, U & 1), ngroups);
-  });
-  chunk_barrier(xb0, touch);
-
-  float cfirst[NB];  // 128-k groups: -s*(128+z) of the first group of an open pair
-
-  // One chunk cc (ring slot U = cc % XB, parity U): start the copy of chunk cc + XB - 1
-  // of x (into the buffer chunk cc - 1 used) and the refill of the weight slot chunk
-  // cc - 1 used, then the chunk's MFMAs and, once a pair of groups is complete, its
-  // zero-point term.
-  auto step = [&](auto u, int cc) __attribute__((always_inline)) {
-    constexpr int U = decltype(u)::value;
-    const int cn = min(cc + XB - 1, last);
-    Body::stage(xring<XB, U + XB - 1>(xb0, xb1, b2, b3, b4, b5), bu, ln, a.K, kb0 + cn, wave);
-    Body::load_w(w[(U + PF - 1) % PF], bu, ln, a.N, kb0 + cn, pair_first(cn, (U + PF - 1) & 1), ngroups);
-    float cneg[GPC][NB];
-    Body::compute(w[U], xring<XB, U>(xb0, xb1, b2, b3, b4, b5), lane, ln, tot, cneg);
-    float cop[NB];
-    if constexpr (GPC == 2) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) cop[nb] = hi ? cneg[1][nb] : cneg[0][nb];
-      Body::apply_pair(w[U].xs, cop, tot);
-    } else if constexpr (U % 2 == 1) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) cop[nb] = hi ? cneg[0][nb] : cfirst[nb];
-      Body::apply_pair(w[U].xs, cop, tot);
-    } else {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) cfirst[nb] = cneg[0][nb];
-      if (cc == last) {  // an odd number of chunks: the last group pairs with nothing
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) cop[nb] = hi ? 0.f : cneg[0][nb];
-        Body::apply_pair(w[U].xs, cop, tot);
-      }
-    }
-    chunk_barrier(xring<XB, U + 1>(xb0, xb1, b2, b3, b4, b5), touch);
-  };
-  for (int c = 0; c < nchunks; c += XB)
-    static_for<XB>([&](auto u) __attribute__((always_inline)) {
-      if (c + decltype(u)::value < nchunks) step(u, c + decltype(u)::value);
+  // The main loop of team T (a compile-time constant, so that its ring buffers are
+  // distinct LDS objects the compiler can tell apart).
+  auto run = [&](auto tc) __attribute__((always_inline)) {
+    constexpr int T = decltype(tc)::value;
+    auto& r0 = T == 0 ? xb0 : b2;
+    auto& r1 = T == 0 ? xb1 : b3;
+    auto& r2 = T == 0 ? b2 : b4;
+    auto& r3 = T == 0 ? b3 : b5;
+    auto ring = [&](auto ic) __attribute__((always_inline)) -> u32x4_t* {
+      return xring<XB, decltype(ic)::value>(r0, r1, r2, r3, b4, b5);
+    };
+    // Prologue: chunks 0 .. XB - 2 of x and of the weights in flight.  Unconditional
+    // loads keep the compiler's count of outstanding loads exact.
+    typename Body::W w[PF];
+    static_for<XB - 1>([&](auto u) __attribute__((always_inline)) {
+      constexpr int U = decltype(u)::value;
+      Body::stage(ring(u), bu, ln, a.K, blk(U), tw);
+      Body::load_w(w[U], bu, ln, a.N, blk(U), pair_first(U, U & 1), ngroups);
     });
-  // The copies past the split's end (never read) are not waited for: they complete
-  // before the workgroup's LDS is released.  `touch` (an xor of the touched values)
-  // only keeps the touching reads alive.
+    chunk_barrier(r0, touch);
+
+    float cfirst[NB];  // 128-k groups: -s*(128+z) of the first group of an open pair
+
+    // One chunk cc (ring slot U = cc % XB, parity U): start the copy of chunk
+    // cc + XB - 1 of x (into the buffer chunk cc - 1 used) and the refill of the weight
+    // slot chunk cc - 1 used, then the chunk's MFMAs and, once a pair of groups is
+    // complete, its zero-point term.
+    auto step = [&](auto u, int cc) __attribute__((always_inline)) {
+      constexpr int U = decltype(u)::value;
+      const int cn = cc + XB - 1;
+      Body::stage(ring(std::integral_constant<int, (U + XB - 1) % XB>{}), bu, ln, a.K, blk(cn), tw);
+      Body::load_w(w[(U + PF - 1) % PF], bu, ln, a.N, blk(cn), pair_first(cn, (U + PF - 1) & 1), ngroups);
+      if (TEAMS == 1 || cc < nchunks) {
+        float cneg[GPC][NB];
+        Body::compute(w[U], ring(u), lane, ln, tot, cneg);
+        float cop[NB];
+        if constexpr (GPC == 2) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) cop[nb] = hi ? cneg[1][nb] : cneg[0][nb];
+          Body::apply_pair(w[U].xs, cop, tot);
+        } else if constexpr (U % 2 == 1) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) cop[nb] = hi ? cneg[0][nb] : cfirst[nb];
+          Body::apply_pair(w[U].xs, cop, tot);
+        } else {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) cfirst[nb] = cneg[0][nb];
+          if (cc == last) {  // an odd number of chunks: the last group pairs with nothing
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) cop[nb] = hi ? 0.f : cneg[0][nb];
+            Body::apply_pair(w[U].xs, cop, tot);
+          }
+        }
+      }
+      chunk_barrier(ring(std::integral_constant<int, (U + 1) % XB>{}), touch);
+    };
+    for (int c = 0; c < nsteps; c += XB)
+      static_for<XB>([&](auto u) __attribute__((always_inline)) {
+        if (c + decltype(u)::value < nsteps) step(u, c + decltype(u)::value);
+      });
+  };
+  if constexpr (TEAMS == 1) {
+    run(std::integral_constant<int, 0>{});
+  } else {
+    if (team == 0)
+      run(std::integral_constant<int, 0>{});
+    else
+      run(std::integral_constant<int, 1>{});
+  }
+  // `touch` (an xor of the touched values) only keeps the touching reads alive.
   if (touch == 0x7FC00001u && a.M < 0) a.y[0] = 0;
+
+  if constexpr (TEAMS == 2) {
+    // Team 1 hands its sums to team 0 through the LDS of its ring (64 KB: 4 wavefronts
+    // x 4 row blocks x 16 registers x 64 lanes).  Copies into the rings issued past the
+    // last chunk may still be landing, so every wavefront first waits for its own.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+    float* red0 = reinterpret_cast<float*>(b2);  // row blocks 0 and 1
+    float* red1 = reinterpret_cast<float*>(b3);  // row blocks 2 and 3
+    auto at = [&](int i, int r) __attribute__((always_inline)) {
+      return ((tw * 2 + (i & 1)) * 16 + r) * kWave + lane;
+    };
+    if (team == 1) {
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) (i < 2 ? red0 : red1)[at(i, r)] = tot[i][0][r];
+    }
+    __syncthreads();
+    if (team == 0) {
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tot[i][0][r] += (i < 2 ? red0 : red1)[at(i, r)];
+    }
+  }
 
   // D layout of the 32x32 MFMA: lane l holds column l % 32 and, in register r, row
   // 8 * (r / 4) + 4 * (l / 32) + r % 4 of the block.
+  if (team == 0) {
 #pragma unroll
-  for (int i = 0; i < MB; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+      for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = 32 * i + 8 * (r / 4) + 4 * hi + (r % 4);
-        if (ok[nb] && m < a.M) store_out(a, wi, m, col[nb], tot[i][nb][r]);
-      }
-  if (wi.nsplit > 1) finish_splitk<WAVES * kWave>(a, ng, WAVES * NB * 32);
+        for (int r = 0; r < 16; ++r) {
+          const int m = 32 * i + 8 * (r / 4) + 4 * hi + (r % 4);
+          if (ok[nb] && m < a.M) store_out(a, wi, m, col[nb], tot[i][nb][r]);
+        }
+  }
+  if (wi.nsplit > 1) finish_splitk<WAVES * kWave>(a, ng, TW * NB * 32);
 }
 
 }  // namespace qmma
@@ -408,7 +477,7 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
 typedef void (*QmmaKernel)(QArgs);
 
 struct MmaVariant {
-  int mb, nb, pf, waves, bits, group;  // pf: depth of the x and weight rings (k_qmma's XB)
+  int mb, nb, pf, waves, teams, bits, group;  // pf: depth of the x and weight rings (k_qmma's XB)
   QmmaKernel fn;
 };
 

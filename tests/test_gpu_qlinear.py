@@ -136,6 +136,25 @@ def test_qlinear_eight_wavefront_groups(M, N, bits, group):
     assert_close(bf16_to_f64(y), y_ref, f"eight wavefronts M={M} N={N} bits={bits} g={group}")
 
 
+@pytest.mark.parametrize("M,N,K,bits,group", [(128, 528, 16384, 3, 128), (65, 1040, 16512, 4, 64),
+                                              (100, 512, 16512, 2, 128)])
+def test_qlinear_two_teams(M, N, K, bits, group):
+    """Long-K launches (at least 128 k-blocks) on two teams of four wavefronts per
+    workgroup, each team on one half of the workgroup's k-blocks (uneven halves when
+    the count is odd), summed through LDS: every output against the oracle."""
+    plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
+    assert plan["mfma_rows"] == 32 and plan["teams"] == 2 and plan["waves"] == 8, plan
+    w = _w(N, K, 330, M, N, K, bits, group)
+    p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+    q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+    x = synth.activations(M, K, 331, M, N, K)
+    ss.subspec_reserve(plan["workspace_bytes"])
+    for _ in range(2):  # the completion counters must be back at zero for the second call
+        y = run_qlinear(p, x.to(DEV))
+        y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, group)
+        assert_close(bf16_to_f64(y), y_ref, f"two teams M={M} N={N} K={K} bits={bits} g={group} plan={plan}")
+
+
 @pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32])
 def test_qlinear_exact_integer_case(path):
     # s=1, z=0, codes in {0,1}, x in {-1,0,1}: every partial sum is a small integer,

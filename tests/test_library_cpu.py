@@ -101,7 +101,7 @@ def test_plan_choices_are_consistent():
                 KB = K // 128
                 assert p["splits"] >= 1 and p["blocks_per_split"] % p["chunk_blocks"] == 0
                 assert (p["splits"] - 1) * p["blocks_per_split"] < KB <= p["splits"] * p["blocks_per_split"]
-                cols = p["waves"] * p["tiles_per_wave"] * 16
+                cols = p["waves"] // p["teams"] * p["tiles_per_wave"] * 16
                 assert p["col_groups"] == -(-N // cols)
                 fg = p["full_groups"]
                 assert 0 <= fg < p["col_groups"]
@@ -134,17 +134,19 @@ def test_mfma_tile_shape_choice():
     at least 192 blocks (four-chunk ring); everything else stays on 16x16x32 tiles.
     Where 256-column groups still cover three quarters of the CUs and K is not split,
     eight wavefronts share a four-chunk ring (if that variant is built for the bit
-    width and group), and from M = 33 such launches take 64-row 32x32x16 tiles too."""
+    width and group), and from M = 33 such launches take 64-row 32x32x16 tiles too.
+    Launches whose K spans at least 128 blocks take two teams of four wavefronts per
+    workgroup (the last tuple entry is then minus the wavefronts of one team)."""
     def shape(M, N, K, bits=3, group=128, path=ss.SUBSPEC_PATH_AUTO):
         p = ss.subspec_qlinear_plan(M, N, K, bits, group, path)
-        return p["mfma_rows"], p["rows"], p["ring_chunks"], p["waves"]
+        return p["mfma_rows"], p["rows"], p["ring_chunks"], p["waves"] // p["teams"] * (1 if p["teams"] == 1 else -1)
     assert shape(128, 55296, 5120) == (32, 128, 4, 8)      # 32B gate|up
     assert shape(128, 55296, 5120, 2, 64) == (32, 128, 4, 8)
     assert shape(128, 55296, 5120, 4, 128) == (32, 128, 2, 4)  # no eight-wavefront 4-bit build
     assert shape(96, 37888, 3584, 4) == (32, 128, 2, 4)     # 7B gate|up: 148 groups of 256
-    assert shape(128, 5120, 27648) == (32, 128, 4, 4)      # 32B down
+    assert shape(128, 5120, 27648) == (32, 128, 2, -4)     # 32B down: two teams of four
+    assert shape(96, 3584, 18944, 4) == (32, 128, 2, -4)   # 7B down
     assert shape(128, 7168, 5120)[0] == 16           # 32B q|k|v
-    assert shape(128, 3584, 18944, 4)[0] == 16       # 7B down
     assert shape(64, 55296, 5120) == (32, 64, 4, 8)        # 32B gate|up, 64-row tiles
     assert shape(33, 55296, 5120, 2, 64) == (32, 64, 4, 8)
     assert shape(48, 55296, 5120, 4, 128) == (32, 64, 4, 8)
