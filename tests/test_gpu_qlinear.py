@@ -155,6 +155,24 @@ def test_qlinear_two_teams(M, N, K, bits, group):
         assert_close(bf16_to_f64(y), y_ref, f"two teams M={M} N={N} K={K} bits={bits} g={group} plan={plan}")
 
 
+@pytest.mark.parametrize("bits,group", [(3, 128), (4, 64), (2, 128)])
+def test_qlinear_single_block_k(bits, group):
+    """K = 128: every split is one k-block starting at block 0, the case in which the
+    32x32 kernel's refill of its second ring slot would ask for the sums of group -1
+    (held at 0, never used); all three paths against the oracle."""
+    N, K = 1040, 128
+    w = _w(N, K, 340, bits, group)
+    p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+    q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+    for path, ms in ((ss.SUBSPEC_PATH_GEMV, (1, 5)), (ss.SUBSPEC_PATH_MFMA16, (3, 64)),
+                     (ss.SUBSPEC_PATH_MFMA32, (17, 100, 128))):
+        for M in ms:
+            x = synth.activations(M, K, 341, M, bits)
+            y = run_qlinear(p, x.to(DEV), path)
+            y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, group)
+            assert_close(bf16_to_f64(y), y_ref, f"K=128 bits={bits} g={group} path={path} M={M}")
+
+
 @pytest.mark.parametrize("path", [ss.SUBSPEC_PATH_GEMV, ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32])
 def test_qlinear_exact_integer_case(path):
     # s=1, z=0, codes in {0,1}, x in {-1,0,1}: every partial sum is a small integer,
