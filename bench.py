@@ -105,11 +105,17 @@ def parse():
 
 # --- kernel identity and measured traffic ----------------------------------------
 
+_COMMENT = re.compile(r"//[^\n]*|/\*.*?\*/", re.S)
+
+
 def kernel_source_hash(family: str = "qlinear") -> str:
+    """Hash of the family's kernel sources with comments and whitespace removed (what
+    the compiler sees), so that measured counters stay attached to unchanged code."""
     h = hashlib.sha256()
     for f in FAMILIES[family]["sources"]:
-        with open(os.path.join(ROOT, "paper_2509_18344_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2509_18344_amd", "csrc", f), encoding="utf-8") as fh:
+            code = _COMMENT.sub(" ", fh.read())
+        h.update(" ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -6,9 +6,12 @@ namespace subspec {
 #define SUBSPEC_QMMA(G, MB, NB, PF, W) {MB, NB, PF, W, 1, 2, G, qmma::k_qmma<2, G, MB, NB, PF, W, 1>}
 #define SUBSPEC_QMMA_TEAMS(G) {4, 1, 2, 8, 2, 2, G, qmma::k_qmma<2, G, 4, 1, 2, 8, 2>}
 
-// Four row blocks (M = 65..128).  Four wavefronts with the ring two chunks deep (two
-// workgroups per CU) or four (one workgroup per CU, for launches split along a long K);
-// eight wavefronts (256 columns, one workgroup per CU) with the ring four chunks deep.
+// Four row blocks (M = 65..128): four wavefronts with the ring two chunks deep (two
+// workgroups per CU) or four (one workgroup per CU); eight wavefronts (256 columns, one
+// workgroup per CU) with the ring four chunks deep.
+// Two row blocks (M = 33..64): eight wavefronts (256 columns) with the ring four chunks
+// deep.  Two teams of four wavefronts, each with a two-chunk ring, on long-K launches
+// above M = 64.
 static const MmaVariant kVariants[] = {
     SUBSPEC_QMMA(128, 4, 1, 2, 4), SUBSPEC_QMMA(128, 4, 1, 4, 4), SUBSPEC_QMMA(128, 4, 1, 4, 8),
     SUBSPEC_QMMA(64, 4, 1, 2, 4),  SUBSPEC_QMMA(64, 4, 1, 4, 4),  SUBSPEC_QMMA(64, 4, 1, 4, 8),

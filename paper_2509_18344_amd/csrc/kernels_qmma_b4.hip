@@ -6,9 +6,12 @@ namespace subspec {
 #define SUBSPEC_QMMA(G, MB, NB, PF, W) {MB, NB, PF, W, 1, 4, G, qmma::k_qmma<4, G, MB, NB, PF, W, 1>}
 #define SUBSPEC_QMMA_TEAMS(G) {4, 1, 2, 8, 2, 4, G, qmma::k_qmma<4, G, 4, 1, 2, 8, 2>}
 
-// Four row blocks (M = 65..128), four wavefronts, the ring two chunks deep (two
-// workgroups per CU) or four (one workgroup per CU, for launches split along a long K).
-// (The eight-wavefront build spills registers at four bits.)
+// Four row blocks (M = 65..128): four wavefronts with the ring two chunks deep (two
+// workgroups per CU) or four (one workgroup per CU).  (The eight-wavefront four-row-block
+// build spills registers at four bits.)
+// Two row blocks (M = 33..64): eight wavefronts (256 columns) with the ring four chunks
+// deep.  Two teams of four wavefronts, each with a two-chunk ring, on long-K launches
+// above M = 64.
 static const MmaVariant kVariants[] = {
     SUBSPEC_QMMA(128, 4, 1, 2, 4), SUBSPEC_QMMA(128, 4, 1, 4, 4), SUBSPEC_QMMA(64, 4, 1, 2, 4),
     SUBSPEC_QMMA(64, 4, 1, 4, 4),

@@ -39,13 +39,12 @@ namespace qmma {
 
 typedef __attribute__((address_space(3))) void* LdsPtr;
 
-// LDS of one workgroup: two chunks of x, each [rows][16 pieces of 8 k] with the
-// pieces of row r permuted by piece ^ (r & 15) (the copy-in writes a row's 16 pieces
-// per 16 lanes and an A fragment reads one piece of 16 consecutive rows per 16 lanes,
-// both conflict free), and the per-group x sums of three chunks.  The two chunk
-// buffers are separate LDS objects on purpose: the copy into one runs while the other
-// is read, and only distinct objects let the compiler see that those reads need not
-// wait for the copy.
+// LDS of one workgroup: a ring of XB chunks of x per team, each [rows][16 pieces of
+// 8 k] with the pieces of row r permuted by piece ^ (r & 15) (the copy-in writes a
+// row's 16 pieces per 16 lanes and an A fragment reads one piece of 16 consecutive rows
+// per 16 lanes, both conflict free).  The chunk buffers are separate LDS objects on
+// purpose: the copy into one runs while another is read, and only distinct objects let
+// the compiler see that those reads need not wait for the copy.
 
 // Code pair P (0..15) of a slice: two bf16 values 128 + q (see device_common.h).
 template <int BITS, int P>
