@@ -96,6 +96,7 @@ struct Tuning {
   // Smallest M at which wide launches take the 32x32 kernel's 64-row eight-wavefront
   // tiles instead of 16x16x32 ones (0 = never).
   int mma8_min_m = 33;
+  int mma8_half_min_m = 48;       // the same where 256-column groups cover only half the CUs
   int mma_teams = 0;              // 32x32 kernel, long-K launches: 1 = one team, 2 = two; 0 = choose
 };
 
@@ -134,6 +135,7 @@ const Tuning& tuning() {
         else if (k == "mma_shape") r.mma_shape = v;
         else if (k == "mma_waves") r.mma_waves = v;
         else if (k == "mma8_min_m") r.mma8_min_m = v;
+        else if (k == "mma8_half_min_m") r.mma8_half_min_m = v;
         else if (k == "mma_teams") r.mma_teams = v;
       }
       pos = end + 1;
@@ -189,14 +191,19 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   const bool wide = (N + 127) / 128 >= device_cus();
   const bool long_k = KB >= 128;
   // 256-column groups (eight wavefronts of the 32x32 kernel) still cover three
-  // quarters of the CUs.
+  // quarters (wide8) or half (half8) of the CUs.
   const bool wide8 = (N + 255) / 256 * 4 >= 3 * device_cus();
+  const bool half8 = (N + 255) / 256 * 2 >= device_cus();
   if (path == SUBSPEC_PATH_MFMA) {
     // Below mma16_max_m, wide unsplit launches still take 64-row 32x32 tiles from
     // mma8_min_m on: 32B gate|up 48.7 against 53.4 us at M = 33, 51.6 against 55.1 at
-    // 48, 53.9 against 59.0 at 64; the short and the long-K launches stay on 16x16x32
-    // (q|k|v at M = 64 27.2 against 19.0 us, down 48.1 against 41.0).
-    const bool tiles64 = tu.mma8_min_m > 0 && M >= tu.mma8_min_m && wide8 && !long_k;
+    // 48, 53.9 against 59.0 at 64; where 256-column groups cover only half the CUs,
+    // from mma8_half_min_m on (7B gate|up, 148 groups: 32.8 against 34.5 us at M = 48,
+    // 35.1 against 37.3 at 64, but 32.4 against 31.1 at 33); the short and the long-K
+    // launches stay on 16x16x32 (q|k|v at M = 64 27.2 against 19.0 us, down 48.1
+    // against 41.0).
+    const bool tiles64 = tu.mma8_min_m > 0 && M >= tu.mma8_min_m && (half8 && !wide8 ? M >= tu.mma8_half_min_m : wide8) &&
+                         !long_k;
     const bool use32 = tu.mma_shape ? tu.mma_shape == 32 : (M > tu.mma16_max_m && (wide || long_k)) || tiles64;
     path = use32 ? SUBSPEC_PATH_MFMA32 : SUBSPEC_PATH_MFMA16;
   }
@@ -236,7 +243,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     c8 = c;
     c8.waves = 8;
     c8.prefetch = tu.mfma_pf ? tu.mfma_pf : 4;
-    use8 = tu.mma_waves == 8 || (!tu.mma_waves && wide8 && !long_k);
+    use8 = tu.mma_waves == 8 || (!tu.mma_waves && (wide8 || (half8 && c.rows == 64)) && !long_k);
     // Long-K launches (split along K, not wide enough for whole groups) take two teams
     // of four wavefronts per workgroup, each on half of the workgroup's k-blocks: two
     // wavefronts per SIMD at the same number of splits (32B down, K = 27648: 61.5

@@ -117,12 +117,13 @@ def test_qlinear_balanced_tail_split(M, bits, group):
 
 @pytest.mark.parametrize("M,N,bits,group", [(128, 49152, 3, 128), (65, 49168, 3, 128), (100, 49168, 2, 64),
                                             (128, 49152, 2, 128), (64, 49152, 3, 128), (33, 49168, 4, 64),
-                                            (48, 49168, 2, 128), (40, 49152, 4, 128)])
+                                            (48, 49168, 2, 128), (40, 49152, 4, 128), (48, 34832, 4, 128),
+                                            (64, 34816, 3, 64)])
 def test_qlinear_eight_wavefront_groups(M, N, bits, group):
     """256-column groups of eight wavefronts sharing one x ring (the plan for wide
-    launches from M = 33: 64-row tiles up to M = 64, 128-row ones above), including a
-    last group with a single 16-column tile (N % 256 = 16): every output against the
-    oracle."""
+    launches from M = 33, and from M = 48 where the groups cover only half the CUs:
+    64-row tiles up to M = 64, 128-row ones above), including a last group with a
+    single 16-column tile (N % 256 = 16): every output against the oracle."""
     K = 384
     plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
     assert plan["mfma_rows"] == 32 and plan["waves"] == 8 and plan["col_groups"] == -(-N // 256), plan

@@ -151,7 +151,9 @@ def test_mfma_tile_shape_choice():
     assert shape(33, 55296, 5120, 2, 64) == (32, 64, 4, 8)
     assert shape(48, 55296, 5120, 4, 128) == (32, 64, 4, 8)
     assert shape(32, 55296, 5120)[0] == 16
-    assert shape(64, 37888, 3584, 4)[0] == 16              # 7B gate|up: not wide enough
+    assert shape(64, 37888, 3584, 4) == (32, 64, 4, 8)     # 7B gate|up: half-wide, from M = 48
+    assert shape(48, 37888, 3584, 4) == (32, 64, 4, 8)
+    assert shape(40, 37888, 3584, 4)[0] == 16
     assert shape(64, 5120, 27648)[0] == 16                 # long K
     assert shape(64, 7168, 5120)[0] == 16                  # q|k|v
     assert shape(17, 512, 256, path=ss.SUBSPEC_PATH_MFMA32) == (32, 128, 4, 4)
