@@ -101,6 +101,9 @@ def test_plan_choices_are_consistent():
                 KB = K // 128
                 assert p["splits"] >= 1 and p["blocks_per_split"] % p["chunk_blocks"] == 0
                 assert (p["splits"] - 1) * p["blocks_per_split"] < KB <= p["splits"] * p["blocks_per_split"]
+                # teams split a workgroup's k-blocks (32x32 tiles only); a layout
+                # mismatch between the binding and the C struct would show here
+                assert p["teams"] == 1 or (p["teams"] == 2 and p["mfma_rows"] == 32 and p["waves"] == 8), p
                 cols = p["waves"] // p["teams"] * p["tiles_per_wave"] * 16
                 assert p["col_groups"] == -(-N // cols)
                 fg = p["full_groups"]
