@@ -137,7 +137,8 @@ def plan_key(plan, bits, group) -> str:
     else:
         family = "k_qgemm_mfma"
         targs = (bits, group, plan["rows"] // 16, plan["tiles_per_wave"], plan["chunk_blocks"], plan["waves"])
-    return dispatch_key(family, targs, plan["grid"] * wg, wg)
+    # the whole launch: row blocks are its grid's y dimension
+    return dispatch_key(family, targs, plan["grid"] * plan["row_blocks"] * wg, wg)
 
 
 def _counter_rows(d, counter):
@@ -228,7 +229,8 @@ def trace_durations(d):
     for fn in files:
         with open(fn) as f:
             for r in csv.DictReader(f):
-                key = library_key(r["Kernel_Name"], int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
+                grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+                key = library_key(r["Kernel_Name"], grid, int(r["Workgroup_Size_X"]))
                 if key:
                     durs[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     return durs
@@ -1035,10 +1037,9 @@ def run_attn(args, torch, ss):
     nbytes = attn_bytes(**c)
     splits, tps = ss.subspec_tree_attention_plan(M, Hq, Hkv, P, T)
     qt = -(-(Hq // Hkv * M) // 16)
-    keys = [f"k_attn_partial<{qt}> grid={splits * 256} wg=256", f"k_attn_combine grid={M * Hq * 128} wg=128"]
-    # the counter files give the whole 2-D grid (splits x Hkv workgroups)
-    tr = [measured_traffic(k, "attn") for k in
-          (f"k_attn_partial<{qt}> grid={splits * 256 * Hkv} wg=256", keys[1])]
+    # keys name the whole grid (k_attn_partial: splits x Hkv workgroups)
+    keys = [f"k_attn_partial<{qt}> grid={splits * 256 * Hkv} wg=256", f"k_attn_combine grid={M * Hq * 128} wg=128"]
+    tr = [measured_traffic(k, "attn") for k in keys]
     achieved = nbytes / (avg_us * 1e-6) / 1e9
     value = nbytes / (ms_per_step * 1e-3) / 1e9
     out_line = {

@@ -100,7 +100,8 @@ typedef struct subspec_plan {
                           least 16384, and for 32 < M <= 64 on launches whose
                           256-column groups cover three quarters of the CUs with K
                           unsplit (measured on the Qwen2.5 shapes)               */
-  int rows;            /* rows computed per workgroup (M rounded up)              */
+  int rows;            /* rows computed per workgroup (M rounded up; with row_blocks
+                          = 2, half of that)                                     */
   int tiles_per_wave;  /* 16-column tiles each wavefront owns                     */
   int waves;           /* wavefronts per workgroup                                */
   int chunk_blocks;    /* 128-k blocks staged in LDS per step                     */
@@ -111,7 +112,7 @@ typedef struct subspec_plan {
                           each; the others are split along K                    */
   int splits;          /* workgroups per split column group; 1 = no partial sums  */
   int blocks_per_split;/* 128-k blocks per split                                  */
-  int grid;            /* total workgroups =
+  int grid;            /* workgroups of one row block =
                           full_groups + (col_groups - full_groups) * splits      */
   size_t workspace_bytes; /* device scratch the call uses: 64 KiB of completion
                              counters, the 32x32 kernel's per-group sums of x, and
@@ -121,6 +122,12 @@ typedef struct subspec_plan {
                           its k-blocks between them (1, or 2: two teams of four on
                           the same columns, summed in LDS); a workgroup covers
                           waves / teams * tiles_per_wave * 16 columns             */
+  int row_blocks;      /* 16-row MFMA tiles: the rows in row_blocks blocks of `rows`
+                          rows each (1 or 2), each block of workgroups an independent
+                          launch along grid y with its own partial sums and
+                          completion counters.  The automatic choice takes 2 for
+                          M > 32 on launches whose column groups number fewer than
+                          the CUs and whose K is under 16384 (q|k|v and o shapes) */
 } subspec_plan;
 
 /* Bytes of the packed code buffer for an N x K projection.  0 on bad arguments. */

@@ -34,7 +34,7 @@ class _Plan(ctypes.Structure):
                 ("full_groups", ctypes.c_int),
                 ("splits", ctypes.c_int), ("blocks_per_split", ctypes.c_int),
                 ("grid", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t),
-                ("teams", ctypes.c_int)]
+                ("teams", ctypes.c_int), ("row_blocks", ctypes.c_int)]
 
 
 class SubspecProj(ctypes.Structure):

@@ -98,6 +98,7 @@ struct Tuning {
   int mma8_min_m = 33;
   int mma8_half_min_m = 48;       // the same where 256-column groups cover only half the CUs
   int mma_teams = 0;              // 32x32 kernel, long-K launches: 1 = one team, 2 = two; 0 = choose
+  int row_split = 0;              // 16x16x32 tiles: 1 = two row blocks where possible, 2 = never; 0 = choose
 };
 
 // Optional overrides for measurement sweeps: SUBSPEC_TUNE="gemv_max_m=4,target=512,...".
@@ -137,6 +138,7 @@ const Tuning& tuning() {
         else if (k == "mma8_min_m") r.mma8_min_m = v;
         else if (k == "mma8_half_min_m") r.mma8_half_min_m = v;
         else if (k == "mma_teams") r.mma_teams = v;
+        else if (k == "row_split") r.row_split = v;
       }
       pos = end + 1;
     }
@@ -324,8 +326,29 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
       }
     }
   }
+  // Row blocks: the 16x16x32 kernel's rows in two blocks of half the tile height, each
+  // a launch of its own along grid y with its own partial sums and counters.  Each
+  // weight tile is then read by two workgroups, but a launch that has to split K needs
+  // half the splits for the same number of workgroups, and the last workgroup of a
+  // column group, which adds the partial sums alone, reads a quarter of them.  Taken
+  // for tiles of 64 rows or more on launches that split a K of under 128 blocks
+  // (q|k|v and o): 32B q|k|v 16.4 against 19.4 us at M = 64, 26.6 against 31.4 at 128,
+  // o 13.6 against 17.2 and 21.9 against 27.4; 7B q|k|v 11.3 against 17.1 at M = 64.
+  // Slower on the long-K down (32B at M = 64: 44.1 against 40.8 us) and on gate|up at
+  // M = 32 (32.2 against 24.9), which keep one block.
+  const bool split_rows = tu.row_split ? tu.row_split == 1
+                                       : c.rows >= 64 && !long_k && groups_of(c) < device_cus();
+  if (c.path == 2 && c.shape == 16 && split_rows && c.rows >= 32 && M > c.rows / 2) {
+    subspec::KernelChoice cr = c;
+    cr.rows = c.rows / 2;
+    cr.row_blocks = 2;
+    cr.chunk = tu.mfma_ch ? tu.mfma_ch : cr.rows == 16 ? 2 : 1;
+    if (variant_exists(cr)) c = cr;
+  }
   const int cols_per_group = c.waves / c.teams * c.nt * subspec::kTileN;
   const int col_groups = groups_of(c);
+  const int units = col_groups * c.row_blocks;  // workgroups of one split
+  const long long part_rows = c.row_blocks > 1 ? static_cast<long long>(c.row_blocks) * c.rows : M;
   const int chunks = (KB + c.chunk - 1) / c.chunk;
 
   // Split K across workgroups only as far as a target workgroup count reaches, and
@@ -337,7 +360,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   // in 13).
   const int per_cu_target = tu.wg_per_cu ? tu.wg_per_cu : 2;
   const int target = tu.target_blocks ? resident : std::min(resident, per_cu_target * device_cus());
-  int splits = std::max(1, target / col_groups);
+  int splits = std::max(1, target / units);
   const double wbytes = static_cast<double>(N) * K * bits / 8 + 4.0 * N * (K / group);
   const double per_split = 8.0 * M * N;
   int cap = tu.partial_div > 0 ? std::max(1, static_cast<int>(wbytes / (tu.partial_div * per_split)))
@@ -345,7 +368,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   // The cap never leaves a CU with fewer than two workgroups: at large M a
   // workgroup's own issue rate, not HBM, bounds it, and partial sums cost less than
   // idle CUs (7B q|k|v at M = 64: 72 workgroups took as long as gate|up).
-  if (tu.fill_cus) cap = std::max(cap, (device_cus() * tu.fill_cus + col_groups - 1) / col_groups);
+  if (tu.fill_cus) cap = std::max(cap, (device_cus() * tu.fill_cus + units - 1) / units);
   splits = std::min(splits, cap);
   if (tu.splits > 0) splits = tu.splits;
   if (c.path == 1) {
@@ -357,18 +380,18 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   }
   // Split-K needs a completion counter per column group and 32-bit offsets into the
   // partial sums.
-  const long long split_bytes = 4ll * M * N;
+  const long long split_bytes = 4ll * part_rows * N;
   auto fit_offsets = [&](int sp) {
     if (sp > 1 && split_bytes * sp >= (1ll << 31))
       sp = std::max(1, static_cast<int>(((1ll << 31) - 1) / split_bytes));
     return sp;
   };
-  if (col_groups > subspec::kSplitCounters) splits = 1;
+  if (units > subspec::kSplitCounters) splits = 1;
   const size_t fixed_ws = subspec::kSplitCounterBytes + xsum_bytes(c, M, K, group);
   auto fit_cap = [&](int sp) {
     if (sp > 1 && ws_cap != SIZE_MAX) {
       const size_t room = ws_cap > fixed_ws ? ws_cap - fixed_ws : 0;
-      const size_t most = room / (static_cast<size_t>(4) * M * N);
+      const size_t most = room / (static_cast<size_t>(4) * part_rows * N);
       if (static_cast<size_t>(sp) > most) sp = static_cast<int>(std::max<size_t>(1, most));
     }
     return sp;
@@ -382,7 +405,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   // a split one.  (A GEMV workgroup that runs a whole group stages all of K.)
   int full_groups = 0;
   const int cus = device_cus();
-  if (splits == 1 && tu.tail && !tu.splits && col_groups <= subspec::kSplitCounters &&
+  if (splits == 1 && tu.tail && !tu.splits && c.row_blocks == 1 && col_groups <= subspec::kSplitCounters &&
       (c.path != 1 || K <= subspec::gemv_max_kspan(c.rows, c.waves, group, cols_per_group))) {
     const int base = col_groups / cus, rem = col_groups % cus;
     const int ts = fit_cap(fit_offsets(std::min(rem ? cus / rem : 0, chunks)));
@@ -410,6 +433,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   p->path = c.path == 1 ? SUBSPEC_PATH_GEMV : SUBSPEC_PATH_MFMA;
   p->mfma_rows = c.path == 2 ? c.shape : 0;
   p->teams = c.teams;
+  p->row_blocks = c.row_blocks;
   p->rows = c.rows;
   p->tiles_per_wave = c.nt;
   p->waves = c.waves;
@@ -425,7 +449,7 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   p->workspace_bytes = 0;
   if (splits > 1 || c.shape == 32)
     p->workspace_bytes = subspec::kSplitCounterBytes + xsum_bytes(c, M, K, group) +
-                         (splits > 1 ? static_cast<size_t>(splits) * M * N * sizeof(float) : 0);
+                         (splits > 1 ? static_cast<size_t>(splits) * part_rows * N * sizeof(float) : 0);
   if (p->workspace_bytes > ws_cap)
     return fail(SUBSPEC_EUNSUPPORTED, "M=%d N=%d K=%d: needs %zu bytes of scratch even unsplit, above the "
                 "%zu available", M, N, K, p->workspace_bytes, ws_cap);
@@ -623,6 +647,10 @@ int qlinear_impl(const void* x, const void* qweight, const void* scales, const v
   a.splits = p.splits;
   a.blocks_per_split = p.blocks_per_split;
   a.span_blocks = p.full_groups > 0 ? a.KB : p.blocks_per_split;
+  if (kc.row_blocks > 1) {
+    a.rb_rows = kc.rows;
+    a.rb_counters = p.col_groups;
+  }
   if (p.workspace_bytes) {
     void* ws = nullptr;
     if (noalloc) {

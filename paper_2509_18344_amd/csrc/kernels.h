@@ -32,6 +32,12 @@ struct QArgs {
   int splits;
   int blocks_per_split;
   int span_blocks;        // largest k-block count of one workgroup (GEMV LDS layout)
+  // Row blocks (launch grid y > 1, 16x16x32 kernel): workgroups with blockIdx.y = r
+  // take rows [r * rb_rows, r * rb_rows + rb_rows) as a launch of their own, with
+  // their own partial sums (splits * rb_rows * N floats per block) and completion
+  // counters (rb_counters per block).  rb_rows = 0: one block of all M rows.
+  int rb_rows;
+  int rb_counters;
 };
 
 struct KernelChoice {
@@ -43,10 +49,11 @@ struct KernelChoice {
   int prefetch = 0;  // ring depth in chunks; 0 = the variant table's choice
   int shape = 0;     // MFMA path: 16 = k_qgemm_mfma (16x16x32), 32 = k_qmma (32x32x16)
   int teams = 1;     // k_qmma: wavefront teams splitting the workgroup's K range
+  int row_blocks = 1;  // k_qgemm_mfma: row blocks of `rows` rows each (launch grid y)
 };
 
 hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QArgs& a,
-                          int grid, hipStream_t st);
+                          int grid, hipStream_t st);  // grid: workgroups per row block
 bool qlinear_variant_exists(const KernelChoice& kc, int bits, int group);
 // Workgroups of this variant that fit on one compute unit (0 if unknown, e.g. no GPU).
 int qlinear_resident_blocks(const KernelChoice& kc, int bits, int group, size_t dyn_lds);

@@ -302,7 +302,8 @@ constexpr int mfma_min_waves() {
 
 template <int BITS, int GROUP, int MT, int NT, int CH, int WAVES, int PF>
 __global__ __launch_bounds__(WAVES * kWave) __attribute__((amdgpu_waves_per_eu(mfma_min_waves<MT, NT>())))
-void k_qgemm_mfma(QArgs a) {
+void k_qgemm_mfma(QArgs args) {
+  const QArgs a = row_block(args);
   static_assert(PF % 2 == 0, "the LDS buffer of a chunk follows the ring slot's parity");
   using Body = MfmaBody<BITS, GROUP, MT, NT, CH, WAVES>;
   constexpr int GPC = Body::GPC;
@@ -736,7 +737,7 @@ hipError_t launch_qlinear(const KernelChoice& kc, int bits, int group, const QAr
   const size_t lds = kc.path == 1 ? gemv_lds_bytes(kc.rows, a.span_blocks * kTileK, group,
                                                    kc.waves * kc.nt * kTileN)
                                   : 0;
-  hipLaunchKernelGGL(v->fn, dim3(grid), dim3(kc.waves * kWave), lds, st, a);
+  hipLaunchKernelGGL(v->fn, dim3(grid, kc.row_blocks), dim3(kc.waves * kWave), lds, st, a);
   return hipGetLastError();
 }
 

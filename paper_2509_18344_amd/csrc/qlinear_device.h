@@ -84,6 +84,22 @@ struct QBuffers {
   }
 };
 
+// The row block of this workgroup (blockIdx.y, see QArgs) as a launch of its own:
+// activations, output, partial sums and completion counters rebased, M cut to the
+// block's rows.
+__device__ __forceinline__ QArgs row_block(const QArgs& in) {
+  QArgs a = in;
+  if (a.rb_rows > 0) {
+    const int r = blockIdx.y, m0 = r * a.rb_rows;
+    a.x += static_cast<size_t>(m0) * a.K;
+    a.y += static_cast<size_t>(m0) * a.N;
+    a.ws += static_cast<size_t>(r) * a.splits * a.rb_rows * a.N;
+    a.cnt += r * a.rb_counters;
+    a.M = min(a.rb_rows, a.M - m0);
+  }
+  return a;
+}
+
 // ---------------------------------------------------------------------------
 // Work of one workgroup (see QArgs): column group ng, k-blocks [kb0, kb_end), and
 // its split index among the nsplit workgroups of that column group.

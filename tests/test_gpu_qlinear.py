@@ -156,6 +156,27 @@ def test_qlinear_two_teams(M, N, K, bits, group):
         assert_close(bf16_to_f64(y), y_ref, f"two teams M={M} N={N} K={K} bits={bits} g={group} plan={plan}")
 
 
+@pytest.mark.parametrize("M,N,K,bits,group", [(33, 1040, 3584, 4, 128), (64, 1040, 3584, 3, 128),
+                                              (100, 528, 5120, 2, 64), (128, 1040, 2560, 3, 64),
+                                              (65, 4624, 3584, 4, 64)])
+def test_qlinear_row_blocks(M, N, K, bits, group):
+    """Short 16x16x32 launches from M = 33 run their rows in two blocks along grid y,
+    each with its own partial sums and completion counters (the second block holding
+    M - rows rows, down to one): every output against the oracle, twice, so that the
+    counters of both blocks must be back at zero for the second call."""
+    plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
+    assert plan["mfma_rows"] == 16 and plan["row_blocks"] == 2 and plan["splits"] > 1, plan
+    w = _w(N, K, 350, M, N, K, bits, group)
+    p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+    q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+    x = synth.activations(M, K, 351, M, N, K)
+    ss.subspec_reserve(plan["workspace_bytes"])
+    for _ in range(2):
+        y = run_qlinear(p, x.to(DEV))
+        y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, group)
+        assert_close(bf16_to_f64(y), y_ref, f"row blocks M={M} N={N} K={K} bits={bits} g={group} plan={plan}")
+
+
 @pytest.mark.parametrize("bits,group", [(3, 128), (4, 64), (2, 128)])
 def test_qlinear_single_block_k(bits, group):
     """K = 128: every split is one k-block starting at block 0, the case in which the

@@ -94,10 +94,13 @@ def test_plan_rejects_bad_shapes(M, N, K, bits, group, path, err):
 
 def test_plan_choices_are_consistent():
     for M in (1, 2, 3, 4, 5, 8, 9, 16, 17, 32, 33, 64, 65, 100, 128):
-        for (N, K) in [(512, 256), (18944, 3584), (3584, 18944), (55296, 5120), (5120, 27648)]:
+        for (N, K) in [(512, 256), (18944, 3584), (3584, 18944), (55296, 5120), (5120, 27648), (7168, 5120)]:
             for bits, group in [(4, 128), (3, 128), (2, 64), (4, 64)]:
                 p = ss.subspec_qlinear_plan(M, N, K, bits, group)
-                assert p["rows"] >= M
+                rb = p["row_blocks"]
+                # row blocks: 16x16x32 tiles only, each block holding at least one row
+                assert rb == 1 or (rb == 2 and p["mfma_rows"] == 16 and p["full_groups"] == 0), p
+                assert p["rows"] * rb >= M > p["rows"] * (rb - 1)
                 KB = K // 128
                 assert p["splits"] >= 1 and p["blocks_per_split"] % p["chunk_blocks"] == 0
                 assert (p["splits"] - 1) * p["blocks_per_split"] < KB <= p["splits"] * p["blocks_per_split"]
@@ -118,7 +121,8 @@ def test_plan_choices_are_consistent():
                 # 32x32 kernel reads (fp32 [M][K/group], 256-byte aligned), then the
                 # splits' fp32 partial sums
                 xs = -(-M * (K // group) * 4 // 256) * 256 if p["mfma_rows"] == 32 else 0
-                partials = p["splits"] * M * N * 4 if p["splits"] > 1 else 0
+                part_rows = 2 * p["rows"] if rb == 2 else M
+                partials = p["splits"] * part_rows * N * 4 if p["splits"] > 1 else 0
                 expect = 65536 + xs + partials if (xs or partials) else 0
                 assert p["workspace_bytes"] == expect, (M, N, K, bits, group, p)
     # 592 column groups on 256 CUs: 512 whole, the last 80 split three ways
@@ -160,6 +164,20 @@ def test_mfma_tile_shape_choice():
     assert shape(64, 5120, 27648)[0] == 16                 # long K
     assert shape(64, 7168, 5120)[0] == 16                  # q|k|v
     assert shape(17, 512, 256, path=ss.SUBSPEC_PATH_MFMA32) == (32, 128, 4, 4)
+    # 16x16x32 launches whose column groups number fewer than the CUs, with K under
+    # 128 blocks, run their rows in two blocks from M = 33 (q|k|v, o); long-K, wide
+    # and M <= 32 launches keep one block
+    def blocks(M, N, K, bits=3, group=128):
+        p = ss.subspec_qlinear_plan(M, N, K, bits, group)
+        return p["row_blocks"], p["rows"]
+    assert blocks(64, 7168, 5120) == (2, 32)              # 32B q|k|v
+    assert blocks(128, 5120, 5120) == (2, 64)             # 32B o
+    assert blocks(33, 4608, 3584, 4) == (2, 32)           # 7B q|k|v
+    assert blocks(100, 3584, 3584, 4) == (2, 64)          # 7B o
+    assert blocks(32, 7168, 5120) == (1, 32)
+    assert blocks(64, 5120, 27648) == (1, 64)             # long K
+    assert blocks(64, 3584, 18944, 4) == (1, 64)
+    assert blocks(40, 37888, 3584, 4) == (1, 64)          # 592 column groups
     assert shape(128, 55296, 5120, path=ss.SUBSPEC_PATH_MFMA16)[0] == 16
     for path in (ss.SUBSPEC_PATH_MFMA16, ss.SUBSPEC_PATH_MFMA32):
         assert ss.subspec_qlinear_plan(40, 512, 256, 4, 64, path)["path"] == ss.SUBSPEC_PATH_MFMA
