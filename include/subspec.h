@@ -99,7 +99,8 @@ typedef struct subspec_plan {
                           every CU with whole 128-column groups or split a K of at
                           least 16384, and for 32 < M <= 64 on launches whose
                           256-column groups cover three quarters of the CUs with K
-                          unsplit (measured on the Qwen2.5 shapes)               */
+                          unsplit or whose K is at least 16384 (measured on the
+                          Qwen2.5 shapes)                                        */
   int rows;            /* rows computed per workgroup (M rounded up; with row_blocks
                           = 2, half of that)                                     */
   int tiles_per_wave;  /* 16-column tiles each wavefront owns                     */
@@ -120,7 +121,8 @@ typedef struct subspec_plan {
                              none of these is needed) */
   int teams;           /* 32-row MFMA tiles: wavefront teams per workgroup that split
                           its k-blocks between them (1, or 2: two teams of four on
-                          the same columns, summed in LDS); a workgroup covers
+                          the same columns, summed in LDS; the automatic choice on
+                          a K of at least 16384 from M = 33); a workgroup covers
                           waves / teams * tiles_per_wave * 16 columns             */
   int row_blocks;      /* 16-row MFMA tiles: the rows in row_blocks blocks of `rows`
                           rows each (1 or 2), each block of workgroups an independent

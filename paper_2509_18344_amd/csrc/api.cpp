@@ -98,6 +98,7 @@ struct Tuning {
   int mma8_min_m = 33;
   int mma8_half_min_m = 48;       // the same where 256-column groups cover only half the CUs
   int mma_teams = 0;              // 32x32 kernel, long-K launches: 1 = one team, 2 = two; 0 = choose
+  int teams64_min_m = 33;         // long-K launches from this M up to 64: 64-row two-team 32x32 tiles
   int row_split = 0;              // 16x16x32 tiles: 1 = two row blocks where possible, 2 = never; 0 = choose
 };
 
@@ -139,6 +140,7 @@ const Tuning& tuning() {
         else if (k == "mma8_half_min_m") r.mma8_half_min_m = v;
         else if (k == "mma_teams") r.mma_teams = v;
         else if (k == "row_split") r.row_split = v;
+        else if (k == "teams64_min_m") r.teams64_min_m = v;
       }
       pos = end + 1;
     }
@@ -201,12 +203,17 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     // mma8_min_m on: 32B gate|up 48.7 against 53.4 us at M = 33, 51.6 against 55.1 at
     // 48, 53.9 against 59.0 at 64; where 256-column groups cover only half the CUs,
     // from mma8_half_min_m on (7B gate|up, 148 groups: 32.8 against 34.5 us at M = 48,
-    // 35.1 against 37.3 at 64, but 32.4 against 31.1 at 33); the short and the long-K
-    // launches stay on 16x16x32 (q|k|v at M = 64 27.2 against 19.0 us, down 48.1
-    // against 41.0).
+    // 35.1 against 37.3 at 64, but 32.4 against 31.1 at 33); the short launches stay on
+    // 16x16x32 (q|k|v at M = 64 27.2 against 19.0 us).  Long-K launches take 64-row
+    // tiles on two teams of four wavefronts from teams64_min_m (below): 32B down 34.5
+    // against 39.3 us at M = 48 and 39.6 against 41.5 at 64, 2-bit g64 36.0 against 43.9
+    // and 40.2 against 46.1; the 7B down about even (25.7 against 25.2 at 48, 26.8
+    // against 27.5 at 64); at M = 32, with half of each tile empty, 30.7 against 27.3.
     const bool tiles64 = tu.mma8_min_m > 0 && M >= tu.mma8_min_m && (half8 && !wide8 ? M >= tu.mma8_half_min_m : wide8) &&
                          !long_k;
-    const bool use32 = tu.mma_shape ? tu.mma_shape == 32 : (M > tu.mma16_max_m && (wide || long_k)) || tiles64;
+    const bool teams64 = tu.teams64_min_m > 0 && long_k && M >= tu.teams64_min_m && M <= 64;
+    const bool use32 =
+        tu.mma_shape ? tu.mma_shape == 32 : (M > tu.mma16_max_m && (wide || long_k)) || tiles64 || teams64;
     path = use32 ? SUBSPEC_PATH_MFMA32 : SUBSPEC_PATH_MFMA16;
   }
   subspec::KernelChoice c{}, c8{};
@@ -250,9 +257,11 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
     // of four wavefronts per workgroup, each on half of the workgroup's k-blocks: two
     // wavefronts per SIMD at the same number of splits (32B down, K = 27648: 61.5
     // against 63.8 us at M = 128, 54.7 against 58.7 at 96; 7B down, K = 18944: 40.5
-    // against 45.7 on 16x16x32 tiles at M = 128).
+    // against 45.7 on 16x16x32 tiles at M = 128).  Each team's ring stays two chunks
+    // deep: four-chunk rings of 64 rows (128 KB of LDS) measured no faster (32B down
+    // 35.2 against 34.5 us at M = 48, 41.3 against 39.6 at 64).
     const bool teams = tu.mma_teams ? tu.mma_teams == 2 : long_k;
-    if (!use8 && teams && c.rows == 128) {
+    if (!use8 && teams) {
       c8 = c;
       c8.waves = 8;
       c8.teams = 2;

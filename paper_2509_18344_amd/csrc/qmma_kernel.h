@@ -231,20 +231,6 @@ struct MmaBody {
   }
 };
 
-// The x ring: XB chunk buffers, separate LDS objects (see above), chunk c in buffer
-// c % XB; selected at compile time.
-template <int XB, int I, int XCH>
-__device__ __forceinline__ u32x4_t* xring(u32x4_t (&b0)[XCH], u32x4_t (&b1)[XCH], u32x4_t (&b2)[XCH],
-                                          u32x4_t (&b3)[XCH], u32x4_t (&b4)[XCH], u32x4_t (&b5)[XCH]) {
-  constexpr int J = I % XB;
-  if constexpr (J == 0) return b0;
-  else if constexpr (J == 1) return b1;
-  else if constexpr (J == 2) return b2;
-  else if constexpr (J == 3) return b3;
-  else if constexpr (J == 4) return b4;
-  else return b5;
-}
-
 // Barrier between chunks.  Each wavefront first reads one element of the buffer the
 // next chunk uses: the compiler then waits for this wavefront's copy into that buffer
 // (and, loads completing in order, for everything issued before it), but not for the
@@ -276,7 +262,7 @@ __global__ __launch_bounds__(WAVES * kWave)
 __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(QArgs a) {
   static_assert(XB % 2 == 0 && XB >= 2 && XB <= 6, "chunk parity (pairs of 128-k groups) follows the ring slot");
   static_assert(WAVES == 4 || WAVES == 8, "wavefronts per workgroup");
-  static_assert(TEAMS == 1 || (TEAMS == 2 && WAVES == 8 && XB == 2 && MB == 4 && NB == 1),
+  static_assert(TEAMS == 1 || (TEAMS == 2 && WAVES == 8 && XB == 2 && (MB == 2 || MB == 4) && NB == 1),
                 "two teams of four wavefronts with two-chunk rings");
   constexpr int TW = WAVES / TEAMS;  // wavefronts per team (its column blocks)
   using Body = MmaBody<BITS, GROUP, MB, NB, TW>;
@@ -284,12 +270,23 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
   constexpr int XCH = Body::XCH;
   constexpr int PF = XB;
   constexpr int NBUF = XB * TEAMS;  // LDS chunk buffers; team t uses [t * XB, t * XB + XB)
+  static_assert(NBUF <= 8, "LDS chunk buffers");
   __shared__ u32x4_t xb0[XCH], xb1[XCH], xb2[NBUF > 2 ? XCH : 1], xb3[NBUF > 3 ? XCH : 1],
-      xb4[NBUF > 4 ? XCH : 1], xb5[NBUF > 5 ? XCH : 1];
-  auto& b2 = reinterpret_cast<u32x4_t(&)[XCH]>(xb2);
-  auto& b3 = reinterpret_cast<u32x4_t(&)[XCH]>(xb3);
-  auto& b4 = reinterpret_cast<u32x4_t(&)[XCH]>(xb4);
-  auto& b5 = reinterpret_cast<u32x4_t(&)[XCH]>(xb5);
+      xb4[NBUF > 4 ? XCH : 1], xb5[NBUF > 5 ? XCH : 1], xb6[NBUF > 6 ? XCH : 1], xb7[NBUF > 7 ? XCH : 1];
+  // Chunk buffer I, selected at compile time: separate LDS objects, so that the
+  // compiler can tell the buffers' accesses apart.
+  auto lds = [&](auto ic) __attribute__((always_inline)) -> u32x4_t* {
+    constexpr int I = decltype(ic)::value;
+    static_assert(I < NBUF, "chunk buffer index");
+    if constexpr (I == 0) return xb0;
+    else if constexpr (I == 1) return xb1;
+    else if constexpr (I == 2) return xb2;
+    else if constexpr (I == 3) return xb3;
+    else if constexpr (I == 4) return xb4;
+    else if constexpr (I == 5) return xb5;
+    else if constexpr (I == 6) return xb6;
+    else return xb7;
+  };
 
   const int lane = threadIdx.x % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
@@ -361,12 +358,9 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
   // distinct LDS objects the compiler can tell apart).
   auto run = [&](auto tc) __attribute__((always_inline)) {
     constexpr int T = decltype(tc)::value;
-    auto& r0 = T == 0 ? xb0 : b2;
-    auto& r1 = T == 0 ? xb1 : b3;
-    auto& r2 = T == 0 ? b2 : b4;
-    auto& r3 = T == 0 ? b3 : b5;
+    // ring slot I of team T: chunk c in slot c % XB
     auto ring = [&](auto ic) __attribute__((always_inline)) -> u32x4_t* {
-      return xring<XB, decltype(ic)::value>(r0, r1, r2, r3, b4, b5);
+      return lds(std::integral_constant<int, T * XB + decltype(ic)::value % XB>{});
     };
     // Prologue: chunks 0 .. XB - 2 of x and of the weights in flight.  Unconditional
     // loads keep the compiler's count of outstanding loads exact.
@@ -376,7 +370,7 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
       Body::stage(ring(u), bu, ln, a.K, blk(U), tw);
       Body::load_w(w[U], bu, ln, a.N, blk(U), pair_first(U, U & 1), ngroups);
     });
-    chunk_barrier(r0, touch);
+    chunk_barrier(ring(std::integral_constant<int, 0>{}), touch);
 
     float cfirst[NB];  // 128-k groups: -s*(128+z) of the first group of an open pair
 
@@ -430,28 +424,30 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
   if (touch == 0x7FC00001u && a.M < 0) a.y[0] = 0;
 
   if constexpr (TEAMS == 2) {
-    // Team 1 hands its sums to team 0 through the LDS of its ring (64 KB: 4 wavefronts
-    // x 4 row blocks x 16 registers x 64 lanes).  Copies into the rings issued past the
-    // last chunk may still be landing, so every wavefront first waits for its own.
+    // Team 1 hands its sums to team 0 through the LDS of its ring (4 wavefronts x MB
+    // row blocks x 16 registers x 64 lanes, the size of two of its chunk buffers: each
+    // holds MB / 2 row blocks).  Copies into the rings issued past the last chunk may
+    // still be landing, so every wavefront first waits for its own.
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
-    float* red0 = reinterpret_cast<float*>(b2);  // row blocks 0 and 1
-    float* red1 = reinterpret_cast<float*>(b3);  // row blocks 2 and 3
+    constexpr int PER = MB / 2;  // row blocks per buffer
+    float* red0 = reinterpret_cast<float*>(lds(std::integral_constant<int, XB>{}));      // row blocks [0, PER)
+    float* red1 = reinterpret_cast<float*>(lds(std::integral_constant<int, XB + 1>{}));  // row blocks [PER, MB)
     auto at = [&](int i, int r) __attribute__((always_inline)) {
-      return ((tw * 2 + (i & 1)) * 16 + r) * kWave + lane;
+      return ((tw * PER + i % PER) * 16 + r) * kWave + lane;
     };
     if (team == 1) {
 #pragma unroll
       for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) (i < 2 ? red0 : red1)[at(i, r)] = tot[i][0][r];
+        for (int r = 0; r < 16; ++r) (i < PER ? red0 : red1)[at(i, r)] = tot[i][0][r];
     }
     __syncthreads();
     if (team == 0) {
 #pragma unroll
       for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) tot[i][0][r] += (i < 2 ? red0 : red1)[at(i, r)];
+        for (int r = 0; r < 16; ++r) tot[i][0][r] += (i < PER ? red0 : red1)[at(i, r)];
     }
   }
 

@@ -138,13 +138,16 @@ def test_qlinear_eight_wavefront_groups(M, N, bits, group):
 
 
 @pytest.mark.parametrize("M,N,K,bits,group", [(128, 528, 16384, 3, 128), (65, 1040, 16512, 4, 64),
-                                              (100, 512, 16512, 2, 128)])
+                                              (100, 512, 16512, 2, 128), (33, 1040, 16384, 4, 128),
+                                              (64, 528, 16512, 3, 64), (48, 512, 16384, 2, 128)])
 def test_qlinear_two_teams(M, N, K, bits, group):
     """Long-K launches (at least 128 k-blocks) on two teams of four wavefronts per
     workgroup, each team on one half of the workgroup's k-blocks (uneven halves when
-    the count is odd), summed through LDS: every output against the oracle."""
+    the count is odd), summed through LDS, on 64-row tiles up to M = 64 and 128-row
+    ones above: every output against the oracle."""
     plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
     assert plan["mfma_rows"] == 32 and plan["teams"] == 2 and plan["waves"] == 8, plan
+    assert plan["rows"] == (64 if M <= 64 else 128), plan
     w = _w(N, K, 330, M, N, K, bits, group)
     p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
     q, s16, z16 = oracle.quantize_minmax(w, bits, group)

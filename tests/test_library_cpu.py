@@ -143,7 +143,8 @@ def test_mfma_tile_shape_choice():
     eight wavefronts share a four-chunk ring (if that variant is built for the bit
     width and group), and from M = 33 such launches take 64-row 32x32x16 tiles too.
     Launches whose K spans at least 128 blocks take two teams of four wavefronts per
-    workgroup (the last tuple entry is then minus the wavefronts of one team)."""
+    workgroup from M = 33 (64-row tiles up to M = 64; the last tuple entry is then minus
+    the wavefronts of one team)."""
     def shape(M, N, K, bits=3, group=128, path=ss.SUBSPEC_PATH_AUTO):
         p = ss.subspec_qlinear_plan(M, N, K, bits, group, path)
         return p["mfma_rows"], p["rows"], p["ring_chunks"], p["waves"] // p["teams"] * (1 if p["teams"] == 1 else -1)
@@ -161,7 +162,9 @@ def test_mfma_tile_shape_choice():
     assert shape(64, 37888, 3584, 4) == (32, 64, 4, 8)     # 7B gate|up: half-wide, from M = 48
     assert shape(48, 37888, 3584, 4) == (32, 64, 4, 8)
     assert shape(40, 37888, 3584, 4)[0] == 16
-    assert shape(64, 5120, 27648)[0] == 16                 # long K
+    assert shape(64, 5120, 27648) == (32, 64, 2, -4)       # long K: 64-row tiles on two teams
+    assert shape(33, 3584, 18944, 4) == (32, 64, 2, -4)
+    assert shape(32, 5120, 27648)[0] == 16
     assert shape(64, 7168, 5120)[0] == 16                  # q|k|v
     assert shape(17, 512, 256, path=ss.SUBSPEC_PATH_MFMA32) == (32, 128, 4, 4)
     # 16x16x32 launches whose column groups number fewer than the CUs, with K under
