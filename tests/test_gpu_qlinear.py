@@ -159,6 +159,26 @@ def test_qlinear_two_teams(M, N, K, bits, group):
         assert_close(bf16_to_f64(y), y_ref, f"two teams M={M} N={N} K={K} bits={bits} g={group} plan={plan}")
 
 
+@pytest.mark.parametrize("M,N,K,bits,group", [(40, 128, 16384, 3, 128), (100, 128, 16384, 4, 64),
+                                              (64, 160, 16384, 2, 128)])
+def test_qlinear_two_teams_one_block_splits(M, N, K, bits, group):
+    """Two teams on splits of a single k-block: team 0 takes the block and team 1 none
+    (it loads in-range blocks it never uses and hands zeros to team 0), on 64- and
+    128-row tiles, with a last column group of one 32-column block (N = 160): every
+    output against the oracle, twice, for the completion counters."""
+    plan = ss.subspec_qlinear_plan(M, N, K, bits, group)
+    assert plan["teams"] == 2 and plan["blocks_per_split"] == 1 and plan["splits"] == K // 128, plan
+    w = _w(N, K, 360, M, N, bits, group)
+    p = device_projection(torch.from_numpy(w).to(DEV), bits, group)
+    q, s16, z16 = oracle.quantize_minmax(w, bits, group)
+    x = synth.activations(M, K, 361, M, N)
+    ss.subspec_reserve(plan["workspace_bytes"])
+    for _ in range(2):
+        y = run_qlinear(p, x.to(DEV))
+        y_ref = oracle.qlinear_ref(synth.bf16_bits(x), q, s16, z16, group)
+        assert_close(bf16_to_f64(y), y_ref, f"one-block team splits M={M} N={N} bits={bits} g={group} plan={plan}")
+
+
 @pytest.mark.parametrize("M,N,K,bits,group", [(33, 1040, 3584, 4, 128), (64, 1040, 3584, 3, 128),
                                               (100, 528, 5120, 2, 64), (128, 1040, 2560, 3, 64),
                                               (65, 4624, 3584, 4, 64)])
