@@ -184,7 +184,6 @@ int make_plan(int M, int N, int K, int bits, int group, int path, subspec_plan* 
   const Tuning& tu = tuning();
   if (path == SUBSPEC_PATH_AUTO) path = (M <= tu.gemv_max_m) ? SUBSPEC_PATH_GEMV : SUBSPEC_PATH_MFMA;
   const int KB = K / subspec::kTileK;
-  const int n_tiles = N / subspec::kTileN;
   // 32x32x16 tiles (k_qmma, 128 rows, 128 columns per workgroup) against 16x16x32
   // (k_qgemm_mfma).  Measured on the Qwen2.5-7B/32B stacks at M = 96 and 128, k_qmma
   // wins where its workgroups fill every CU without splitting K (gate|up: 7B 52.8
@@ -827,14 +826,14 @@ int subspec_stack_capture(const subspec_proj* projs, int nproj, int bits, int gr
   hipGraph_t graph = nullptr;
   e = hipStreamEndCapture(stream, &graph);
   if (rc) {
-    if (graph) hipGraphDestroy(graph);
+    if (graph) (void)hipGraphDestroy(graph);  // the capture error is the one reported
     return rc;
   }
   if (e != hipSuccess) return hip_fail(e, "hipStreamEndCapture");
   hipGraphExec_t exec = nullptr;
   e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
   if (e != hipSuccess) {
-    hipGraphDestroy(graph);
+    (void)hipGraphDestroy(graph);  // the instantiation error is the one reported
     return hip_fail(e, "hipGraphInstantiate");
   }
   subspec_graph* g = new subspec_graph;
