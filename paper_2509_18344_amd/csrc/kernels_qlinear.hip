@@ -415,17 +415,56 @@ void k_qgemm_mfma(QArgs args) {
     if (wave >= MT) run(std::integral_constant<int, -1>{});
   }
 
-  // D layout of 16x16 MFMA: lane holds column lane%16, rows 4*(lane/16) + r.
+  // D layout of 16x16 MFMA: lane holds column lane%16, rows 4*(lane/16) + r.  The
+  // stores go through a buffer resource over the output (bf16 y, or this split's fp32
+  // partial sums) with the whole offset in the vector offset, which the range check
+  // covers: rows at or past M and the lanes of a tile past N (given an offset outside
+  // the resource) are dropped.  All offsets stay below 2^31 when the tile's rows span
+  // less than 2 GiB; larger outputs take per-element stores.
   const int quarter = lane >> 4;
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  const bool split = wi.nsplit > 1;
+  const uint32_t esz = split ? 4 : 2;
+  if (static_cast<uint64_t>(16 * MT) * a.N * esz < (1ull << 31)) {
+    const uint32_t rowb = static_cast<uint32_t>(a.N) * esz;
+    const uint32_t out_bytes = static_cast<uint32_t>(a.M) * rowb;
+    const __amdgpu_buffer_rsrc_t out =
+        split ? buffer_rsrc(a.ws + static_cast<size_t>(wi.split) * a.M * a.N, out_bytes) : buffer_rsrc(a.y, out_bytes);
+    constexpr uint32_t kOutside = 0x80000000u;
+    uint32_t voff[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t)
+      voff[t] = ok[t] ? static_cast<uint32_t>(col[t]) * esz + static_cast<uint32_t>(4 * quarter) * rowb : kOutside;
+    auto store_all = [&](auto splitc) __attribute__((always_inline)) {
+      constexpr bool SPLIT = decltype(splitc)::value;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = 16 * mt + 4 * quarter + r;
-        if (ok[t] && m < a.M) store_out(a, wi, m, col[t], tot[mt][t][r]);
-      }
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const uint32_t off = voff[t] + static_cast<uint32_t>(16 * mt + r) * rowb;
+            const float v = tot[mt][t][r];  // a plain value: bit casts of a vector element misbehave
+            if constexpr (SPLIT)
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), out, off, 0, kCachePolicyAgent);
+            else
+              __builtin_amdgcn_raw_buffer_store_b16(float_to_bf16_bits(v), out, off, 0, 0);
+          }
+    };
+    if (split)
+      store_all(std::true_type{});
+    else
+      store_all(std::false_type{});
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = 16 * mt + 4 * quarter + r;
+          if (ok[t] && m < a.M) store_out(a, wi, m, col[t], tot[mt][t][r]);
+        }
+  }
   if (wi.nsplit > 1) finish_splitk<WAVES * kWave>(a, ng, WAVES * NT * kTileN);
 }
 

@@ -452,17 +452,58 @@ __attribute__((amdgpu_waves_per_eu(WAVES == 8 || XB <= 2 ? 2 : 1))) void k_qmma(
   }
 
   // D layout of the 32x32 MFMA: lane l holds column l % 32 and, in register r, row
-  // 8 * (r / 4) + 4 * (l / 32) + r % 4 of the block.
+  // 8 * (r / 4) + 4 * (l / 32) + r % 4 of the block.  The stores go through a buffer
+  // resource over the output (bf16 y, or this split's fp32 partial sums) with the
+  // whole offset in the vector offset, which the range check covers (the scalar
+  // offset is not checked): rows at or past M fall outside the resource and are
+  // dropped, and so are the lanes of a column block past N, given an offset outside
+  // it.  All offsets stay below 2^31 (no wrap-around into the range) when the tile's
+  // rows span less than 2 GiB; larger outputs take per-element stores.
   if (team == 0) {
-#pragma unroll
-    for (int i = 0; i < MB; ++i)
+    const bool split = wi.nsplit > 1;
+    const uint32_t esz = split ? 4 : 2;
+    const uint64_t out_bytes = static_cast<uint64_t>(a.M) * a.N * esz;
+    if (static_cast<uint64_t>(32 * MB) * a.N * esz < (1ull << 31)) {
+      const uint32_t rowb = static_cast<uint32_t>(a.N) * esz;
+      const __amdgpu_buffer_rsrc_t out =
+          split ? buffer_rsrc(a.ws + static_cast<size_t>(wi.split) * a.M * a.N, static_cast<uint32_t>(out_bytes))
+                : buffer_rsrc(a.y, static_cast<uint32_t>(out_bytes));
+      constexpr uint32_t kOutside = 0x80000000u;
+      uint32_t voff[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
+        voff[nb] = ok[nb] ? static_cast<uint32_t>(col[nb]) * esz + static_cast<uint32_t>(4 * hi) * rowb : kOutside;
+      auto store_all = [&](auto splitc) __attribute__((always_inline)) {
+        constexpr bool SPLIT = decltype(splitc)::value;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = 32 * i + 8 * (r / 4) + 4 * hi + (r % 4);
-          if (ok[nb] && m < a.M) store_out(a, wi, m, col[nb], tot[i][nb][r]);
-        }
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const uint32_t off = voff[nb] + static_cast<uint32_t>(32 * i + 8 * (r / 4) + (r % 4)) * rowb;
+              const float v = tot[i][nb][r];  // a plain value: bit casts of a vector element misbehave
+              if constexpr (SPLIT)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), out, off, 0, kCachePolicyAgent);
+              else
+                __builtin_amdgcn_raw_buffer_store_b16(float_to_bf16_bits(v), out, off, 0, 0);
+            }
+      };
+      if (split)
+        store_all(std::true_type{});
+      else
+        store_all(std::false_type{});
+    } else {
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = 32 * i + 8 * (r / 4) + 4 * hi + (r % 4);
+            if (ok[nb] && m < a.M) store_out(a, wi, m, col[nb], tot[i][nb][r]);
+          }
+    }
   }
   if (wi.nsplit > 1) finish_splitk<WAVES * kWave>(a, ng, TW * NB * 32);
 }
